@@ -1,0 +1,211 @@
+/*
+ * hilberta.h -- C ABI of libhilberta.so, the HilbertA hot path on AMD
+ * Instinct MI355X (gfx950).
+ *
+ * HilbertA (arXiv 2509.26538) orders the image tokens of a diffusion
+ * transformer along a Hilbert curve, attends densely inside contiguous tiles
+ * of that sequence, slides the tile boundaries by a fixed offset per layer
+ * without moving any data, and lets every token attend a small central
+ * shared region and the text tokens.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Ownership  The caller allocates every buffer (device memory unless stated)
+ *            and keeps ownership; the library keeps no pointer after a call
+ *            returns and allocates no device memory in these entry points.
+ * Streams    `stream` is a hipStream_t (NULL = the default stream).  Every
+ *            device-side call is asynchronous on that stream.
+ * Errors     Functions return HILBERTA_OK (0) or a negative code.  Every
+ *            argument is validated on the host before anything is launched,
+ *            so an error leaves all outputs untouched and launches nothing.
+ *            hilberta_last_error() returns a message for the calling thread's
+ *            last failing call.  No C++ exception crosses this interface.
+ * Sequence   The attention sequence of one (batch, head) is N_tot = n_txt +
+ *            N_img tokens: text tokens at [0, n_txt), then the image tokens
+ *            in Hilbert order at [n_txt, N_tot) (Appendix A places the text
+ *            as a global prefix).  Shared-region tokens keep their Hilbert
+ *            slots inside the image span.
+ * Tensors    Q, K, V, O are [B, H, N_tot, D] with element strides given as
+ *            {batch, head, row, dim}; the dim stride must be 1 and the other
+ *            strides multiples of 8 elements (16-byte rows for bf16).
+ */
+#ifndef HILBERTA_H
+#define HILBERTA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HILBERTA_OK 0
+#define HILBERTA_EINVAL (-1)       /* null pointer, size or stride out of range */
+#define HILBERTA_EUNSUPPORTED (-2) /* valid but not supported: grid shape, D, dtype, alignment */
+#define HILBERTA_ECAPACITY (-3)    /* output or workspace too small; *needed is set */
+#define HILBERTA_EHIP (-4)         /* a HIP runtime call failed */
+
+/* element types */
+#define HILBERTA_F32 0
+#define HILBERTA_BF16 1
+
+/* first word of every schedule table */
+#define HILBERTA_SCHEDULE_MAGIC 0x48424131
+
+/*
+ * Geometry of one HilbertA attention layer stack.
+ *   grid_h, grid_w   latent grid; must be square with a power-of-two side in
+ *                    [2, 32768] (the Hilbert curve of §3.1 lives on 2^k grids)
+ *   n_txt            text tokens placed before the image tokens (>= 0)
+ *   tile             N_T, tokens per tile; divides grid_h*grid_w (§3.2)
+ *   delta            per-layer advance Delta of the tile boundaries (>= 0);
+ *                    the paper sets Delta = N_T / L for a slide cycle L (§3.2)
+ *   shared_h/_w      central shared region (§3.3): image rows and columns in
+ *                    [(side - s)/2, (side - s)/2 + s), integer halving; 0 x 0
+ *                    disables it.  shared_h + shared_w must be <= 255.
+ * The sequence must satisfy n_txt + grid_h*grid_w < 2^31.
+ */
+typedef struct hilberta_config {
+    int32_t grid_h;
+    int32_t grid_w;
+    int32_t n_txt;
+    int32_t tile;
+    int32_t delta;
+    int32_t shared_h;
+    int32_t shared_w;
+} hilberta_config;
+
+/* Library version (major*10000 + minor*100 + patch). Host only. */
+int hilberta_version(void);
+
+/* Message for the calling thread's last failing call ("" if none). Host only. */
+const char* hilberta_last_error(void);
+
+/*
+ * hilberta_build_perm -- the Hilbert linearisation pi of §3.1.
+ *   perm[d] = y*grid_w + x, where (x = column, y = row) is the cell at Hilbert
+ *   position d, for d in [0, grid_h*grid_w).  The curve starts at (0, 0) and
+ *   ends at (grid_w-1, 0).  If inv_or_null is not NULL, inv[perm[d]] = d.
+ *   perm, inv: device int32 arrays of grid_h*grid_w entries.
+ * Errors: EINVAL (perm NULL), EUNSUPPORTED (grid not square power of two in
+ * [2, 32768]).
+ */
+int hilberta_build_perm(int32_t grid_h, int32_t grid_w, int32_t* perm,
+                        int32_t* inv_or_null, void* stream);
+
+/*
+ * hilberta_permute -- the token gather of §3.4, applied once at the input:
+ *   y[b, d, :] = x[b, perm[d], :]   for b < batch, d < n, all `channels`.
+ * hilberta_unpermute -- its inverse, applied once at the output:
+ *   y[b, perm[d], :] = x[b, d, :].
+ *   x, y      device tensors of `dtype`; rows of `channels` contiguous
+ *             elements; strides in elements.  To leave text rows alone, pass
+ *             pointers offset to the first image row.  x and y must not
+ *             overlap.
+ *   perm      device int32[n], a permutation of [0, n) (e.g. from
+ *             hilberta_build_perm).  Entries outside [0, n) are not read
+ *             through: such rows are skipped by the gather and the scatter.
+ * Errors: EINVAL (NULL pointer, negative size, row stride < channels),
+ * EUNSUPPORTED (dtype).
+ */
+int hilberta_permute(const void* x, void* y, const int32_t* perm, int64_t batch,
+                     int64_t n, int64_t channels, int64_t x_batch_stride,
+                     int64_t x_row_stride, int64_t y_batch_stride,
+                     int64_t y_row_stride, int dtype, void* stream);
+int hilberta_unpermute(const void* x, void* y, const int32_t* perm, int64_t batch,
+                       int64_t n, int64_t channels, int64_t x_batch_stride,
+                       int64_t x_row_stride, int64_t y_batch_stride,
+                       int64_t y_row_stride, int dtype, void* stream);
+
+/*
+ * hilberta_schedule_words -- int32 words of the schedule table for cfg.
+ * Host only; validates cfg like hilberta_schedule.
+ */
+int hilberta_schedule_words(const hilberta_config* cfg, int64_t* words);
+
+/*
+ * hilberta_schedule -- the per-layer tile schedule of §3.2 and the shared
+ * runs of §3.3, written to device memory `sched` (int32[capacity]).
+ *   Layer l slides the boundaries by o = (l*delta) mod N_img: image position
+ *   p has tile label floor((p + l*delta)/N_T) mod T, queries and keys of equal
+ *   label attend each other, and the wrap-around tile is read with modular
+ *   indexing (§3.2), never copied.
+ *   Table layout (int32 words):
+ *     [0] HILBERTA_SCHEDULE_MAGIC  [1] n_txt  [2] N_img  [3] N_T  [4] T
+ *     [5] o  [6] n_spans  [7] n_shared  [8] layer  [9] grid_h  [10] grid_w
+ *     [11] span capacity C = shared_h + shared_w + 1 (0 without a region)
+ *     [12 + 4q .. 12 + 4q + 3], q < T: tile q as (start, len1, len2, ns):
+ *         its tokens are [start, start + len1) and, when it wraps past the
+ *         end of the sequence, [n_txt, n_txt + len2); start is a sequence
+ *         position; ns = shared tokens inside the tile.
+ *     [12 + 4T + 2s, +1], s < C: shared run s as (start, len), sequence
+ *         positions, ascending, maximal; zero past n_spans.
+ *   The table has exactly hilberta_schedule_words(cfg) words.
+ * Errors: EINVAL (NULL, layer < 0), EUNSUPPORTED (cfg out of range),
+ * ECAPACITY (capacity too small; *needed set if needed is not NULL).
+ */
+int hilberta_schedule(const hilberta_config* cfg, int32_t layer, int32_t* sched,
+                      int64_t capacity, int64_t* needed, void* stream);
+
+/*
+ * hilberta_attn_workspace_bytes -- device workspace hilberta_attn_fwd needs
+ * for its split key passes over dense rows.  Host only.
+ */
+int hilberta_attn_workspace_bytes(const hilberta_config* cfg, int64_t batch,
+                                  int64_t heads, int64_t head_dim, int dtype,
+                                  int64_t* bytes);
+
+/*
+ * hilberta_attn_fwd -- HilbertA sparse attention forward (§3.2-§3.4,
+ * Appendix A, Algorithm 1), one launch over all rows:
+ *   rows of text and shared tokens attend all N_tot keys;
+ *   every other image row attends the text keys, the shared keys and the
+ *   keys of its own slid tile, each key once;
+ *   O = softmax(scale * Q K^T restricted to those keys) V, and optionally
+ *   lse = ln sum exp(scale * q.k) over the same keys (natural log).
+ *   sched      device table from hilberta_schedule(cfg, layer, ...); it
+ *              selects the layer.  A table for another cfg gives wrong
+ *              results but no out-of-bounds access.
+ *   q,k,v,o    device [batch, heads, N_tot, head_dim] with strides
+ *              {batch, head, row, dim} in elements, dim stride 1; o may not
+ *              overlap q, k or v.
+ *   lse_or_null device float[batch*heads*N_tot] (row-major b, h, n) or NULL.
+ *   head_dim   64 or 128.  dtype HILBERTA_BF16 (fp32 accumulation, P rounded
+ *              to bf16 for PV, bf16 output) or HILBERTA_F32 (fp32 throughout).
+ *   scale      softmax scale, usually 1/sqrt(head_dim).
+ *   workspace  device scratch of at least hilberta_attn_workspace_bytes, or
+ *              NULL with workspace_bytes 0 to run without split key passes.
+ * With batch*heads == 0 nothing is read or written and the tensor pointers
+ * may be NULL.
+ * Errors: EINVAL, EUNSUPPORTED (head_dim, dtype, stride alignment),
+ * ECAPACITY (workspace given but too small), EHIP.
+ */
+int hilberta_attn_fwd(const hilberta_config* cfg, const int32_t* sched,
+                      const void* q, const void* k, const void* v, void* o,
+                      float* lse_or_null, int64_t batch, int64_t heads,
+                      int64_t head_dim, const int64_t q_strides[4],
+                      const int64_t k_strides[4], const int64_t v_strides[4],
+                      const int64_t o_strides[4], int dtype, float scale,
+                      void* workspace, int64_t workspace_bytes, void* stream);
+
+/* dense_attn_workspace_bytes -- workspace for dense_attn_fwd. Host only. */
+int dense_attn_workspace_bytes(int64_t batch, int64_t heads, int64_t n,
+                               int64_t head_dim, int dtype, int64_t* bytes);
+
+/*
+ * dense_attn_fwd -- full softmax attention over all n keys for every row:
+ * the baseline HilbertA is measured against (Table 1's dense rows), built
+ * from the same kernels and layout as hilberta_attn_fwd.  Arguments as for
+ * hilberta_attn_fwd with N_tot = n and no schedule.
+ */
+int dense_attn_fwd(const void* q, const void* k, const void* v, void* o,
+                   float* lse_or_null, int64_t batch, int64_t heads, int64_t n,
+                   int64_t head_dim, const int64_t q_strides[4],
+                   const int64_t k_strides[4], const int64_t v_strides[4],
+                   const int64_t o_strides[4], int dtype, float scale,
+                   void* workspace, int64_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HILBERTA_H */

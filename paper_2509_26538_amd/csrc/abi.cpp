@@ -1,0 +1,386 @@
+// Host side of the C ABI declared in include/hilberta.h: argument
+// validation, the work plan of an attention launch, and the launches.
+// Every check runs before the first HIP call, so all error paths can be
+// exercised on a machine without a GPU.
+#include "hilberta.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "internal.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int hip_status(hipError_t e, const char* what) {
+    if (e == hipSuccess) return HILBERTA_OK;
+    return fail(HILBERTA_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+
+int check_config(const hilberta_config* c) {
+    if (!c) return fail(HILBERTA_EINVAL, "config is NULL");
+    if (c->grid_h != c->grid_w)
+        return fail(HILBERTA_EUNSUPPORTED, "grid %dx%d is not square", c->grid_h, c->grid_w);
+    if (!pow2(c->grid_w) || c->grid_w < 2 || c->grid_w > 32768)
+        return fail(HILBERTA_EUNSUPPORTED, "grid side %d is not a power of two in [2, 32768]",
+                    c->grid_w);
+    const int64_t n_img = (int64_t)c->grid_h * c->grid_w;
+    if (c->n_txt < 0) return fail(HILBERTA_EINVAL, "n_txt %d < 0", c->n_txt);
+    if (c->n_txt + n_img > 0x7fffffffLL)
+        return fail(HILBERTA_EUNSUPPORTED, "sequence of %lld tokens is too long",
+                    (long long)(c->n_txt + n_img));
+    if (c->tile < 1 || n_img % c->tile)
+        return fail(HILBERTA_EUNSUPPORTED, "tile %d does not divide %lld image tokens", c->tile,
+                    (long long)n_img);
+    if (c->delta < 0) return fail(HILBERTA_EINVAL, "delta %d < 0", c->delta);
+    if (c->shared_h < 0 || c->shared_w < 0 || c->shared_h > c->grid_h || c->shared_w > c->grid_w)
+        return fail(HILBERTA_EINVAL, "shared region %dx%d outside the grid", c->shared_h, c->shared_w);
+    if ((c->shared_h == 0) != (c->shared_w == 0))
+        return fail(HILBERTA_EINVAL, "shared region %dx%d: both sides or neither must be zero",
+                    c->shared_h, c->shared_w);
+    if (c->shared_h + c->shared_w > 255)
+        return fail(HILBERTA_EUNSUPPORTED, "shared region %dx%d: shared_h + shared_w must be <= 255",
+                    c->shared_h, c->shared_w);
+    return HILBERTA_OK;
+}
+
+int64_t span_capacity(const hilberta_config* c) {
+    return c->shared_h * c->shared_w ? c->shared_h + c->shared_w + 1 : 0;
+}
+
+int64_t schedule_words(const hilberta_config* c) {
+    const int64_t n_img = (int64_t)c->grid_h * c->grid_w;
+    return 12 + 4 * (n_img / c->tile) + 2 * span_capacity(c);
+}
+
+struct Tensor4 {
+    const void* p;
+    const int64_t* s;
+    const char* name;
+};
+
+int check_attn_common(const Tensor4* t, int n_t, int64_t batch, int64_t heads, int64_t n,
+                      int64_t head_dim, int dtype, float scale) {
+    if (batch < 0 || heads < 0) return fail(HILBERTA_EINVAL, "negative batch or heads");
+    if (head_dim != 64 && head_dim != 128)
+        return fail(HILBERTA_EUNSUPPORTED, "head_dim %lld not in {64, 128}", (long long)head_dim);
+    if (dtype != HILBERTA_F32 && dtype != HILBERTA_BF16)
+        return fail(HILBERTA_EUNSUPPORTED, "dtype %d", dtype);
+    if (!(scale > 0.f) || !std::isfinite(scale))
+        return fail(HILBERTA_EINVAL, "scale must be finite and > 0");
+    if (batch * heads > 0x7fffffffLL) return fail(HILBERTA_EUNSUPPORTED, "too many heads");
+    if (batch * heads == 0 || n == 0) return HILBERTA_OK;  // nothing is read or written
+    const int64_t align = dtype == HILBERTA_BF16 ? 8 : 4;  // elements in 16 bytes
+    for (int i = 0; i < n_t; ++i) {
+        if (!t[i].p) return fail(HILBERTA_EINVAL, "%s is NULL", t[i].name);
+        if (!t[i].s) return fail(HILBERTA_EINVAL, "%s strides are NULL", t[i].name);
+        if (t[i].s[3] != 1)
+            return fail(HILBERTA_EUNSUPPORTED, "%s: dim stride must be 1", t[i].name);
+        for (int j = 0; j < 3; ++j) {
+            if (t[i].s[j] < 0) return fail(HILBERTA_EINVAL, "%s: negative stride", t[i].name);
+            if (t[i].s[j] % align)
+                return fail(HILBERTA_EUNSUPPORTED, "%s: stride %lld is not a multiple of %lld elements",
+                            t[i].name, (long long)t[i].s[j], (long long)align);
+        }
+        if ((uintptr_t)t[i].p % 16)
+            return fail(HILBERTA_EUNSUPPORTED, "%s is not 16-byte aligned", t[i].name);
+    }
+    return HILBERTA_OK;
+}
+
+// The work plan of one attention launch (see AttnArgs).  Depends only on the
+// shapes, so the workspace query and the launch agree.
+struct Plan {
+    int64_t n_dense_rows, dense_row_blocks, n_chunks, chunk_keys, sparse_blocks, items_per_bh,
+        total_items, ws_bytes;
+};
+
+// Split long dense rows into key chunks about as long as a sparse item's key
+// list, so that no workgroup runs far longer than the rest; for the dense
+// baseline, split only when the rows alone would not fill the GPU a few times.
+Plan make_plan(bool sparse, int64_t n_txt, int64_t n_img, int64_t n_shared, int64_t tile,
+               int64_t n_tot, int64_t bh, int64_t head_dim, bool allow_split) {
+    Plan p{};
+    const int64_t bn = hilberta::kBlockN, bm = hilberta::kBlockM;
+    int64_t chunk = round_up(n_tot, bn);
+    if (sparse) {
+        p.n_dense_rows = n_txt + n_shared;
+        p.sparse_blocks = ceil_div(n_img, bm);
+        const int64_t sparse_keys = round_up(n_txt, bn) + round_up(n_shared, bn) +
+                                    round_up(tile < n_img ? tile : n_img, bn);
+        chunk = round_up(sparse_keys > 512 ? sparse_keys : 512, bn);
+    } else {
+        p.n_dense_rows = n_tot;
+        p.sparse_blocks = 0;
+        const int64_t row_items = ceil_div(n_tot, bm) * bh;
+        const int64_t want = 2048;  // about four rounds of workgroups on 256 CUs
+        if (row_items < want) {
+            int64_t k = ceil_div(want, row_items);
+            const int64_t kmax = ceil_div(n_tot, 512);
+            if (k > kmax) k = kmax;
+            if (k < 1) k = 1;
+            chunk = round_up(ceil_div(n_tot, k), bn);
+        }
+    }
+    if (chunk > round_up(n_tot, bn)) chunk = round_up(n_tot, bn);
+    if (!allow_split || chunk < bn) chunk = round_up(n_tot, bn);
+    p.chunk_keys = chunk;
+    p.n_chunks = n_tot > 0 ? ceil_div(n_tot, chunk) : 1;
+    if (p.n_dense_rows == 0) p.n_chunks = 1;
+    p.dense_row_blocks = ceil_div(p.n_dense_rows, bm);
+    p.items_per_bh = p.dense_row_blocks * p.n_chunks + p.sparse_blocks;
+    p.total_items = p.items_per_bh * bh;
+    p.ws_bytes = p.n_chunks > 1 ? bh * p.n_chunks * p.n_dense_rows * (head_dim + 2) * 4 : 0;
+    return p;
+}
+
+int run_attention(bool sparse, const hilberta_config* cfg, const int32_t* sched, const void* q,
+                  const void* k, const void* v, void* o, float* lse, int64_t batch, int64_t heads,
+                  int64_t n_tot, int64_t head_dim, const int64_t* qs, const int64_t* ks,
+                  const int64_t* vs, const int64_t* os, int dtype, float scale, void* ws,
+                  int64_t ws_bytes, void* stream) {
+    const Tensor4 t[4] = {{q, qs, "q"}, {k, ks, "k"}, {v, vs, "v"}, {o, os, "o"}};
+    int rc = check_attn_common(t, 4, batch, heads, n_tot, head_dim, dtype, scale);
+    if (rc) return rc;
+    if (ws_bytes < 0 || (ws == nullptr && ws_bytes != 0))
+        return fail(HILBERTA_EINVAL, "workspace NULL with %lld bytes", (long long)ws_bytes);
+    if (ws && (uintptr_t)ws % 16) return fail(HILBERTA_EUNSUPPORTED, "workspace is not 16-byte aligned");
+    int64_t n_txt = 0, n_img = n_tot, n_shared = 0, tile = n_tot, n_tiles = 1, cap = 0;
+    if (sparse) {
+        n_txt = cfg->n_txt;
+        n_img = (int64_t)cfg->grid_h * cfg->grid_w;
+        n_shared = (int64_t)cfg->shared_h * cfg->shared_w;
+        tile = cfg->tile;
+        n_tiles = n_img / tile;
+        cap = span_capacity(cfg);
+    }
+    if (n_tot > 0x7fffffffLL) return fail(HILBERTA_EUNSUPPORTED, "sequence too long");
+    const int64_t bh = batch * heads;
+    if (bh == 0 || n_tot == 0) return HILBERTA_OK;
+    Plan p = make_plan(sparse, n_txt, n_img, n_shared, tile, n_tot, bh, head_dim, ws != nullptr);
+    if (ws && ws_bytes < p.ws_bytes)
+        return fail(HILBERTA_ECAPACITY, "workspace of %lld bytes, %lld needed", (long long)ws_bytes,
+                    (long long)p.ws_bytes);
+    if (p.total_items > 0x7fffffffLL) return fail(HILBERTA_EUNSUPPORTED, "too many work items");
+
+    hilberta::AttnArgs a{};
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.o = o;
+    a.lse = lse;
+    a.ws = static_cast<float*>(ws);
+    a.sched = sched;
+    a.q_sb = qs[0]; a.q_sh = qs[1]; a.q_sr = qs[2];
+    a.k_sb = ks[0]; a.k_sh = ks[1]; a.k_sr = ks[2];
+    a.v_sb = vs[0]; a.v_sh = vs[1]; a.v_sr = vs[2];
+    a.o_sb = os[0]; a.o_sh = os[1]; a.o_sr = os[2];
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.heads = (int32_t)heads;
+    a.n_tot = (int32_t)n_tot;
+    a.n_txt = (int32_t)n_txt;
+    a.n_img = (int32_t)n_img;
+    a.tile = (int32_t)tile;
+    a.n_tiles = (int32_t)n_tiles;
+    a.span_cap = (int32_t)cap;
+    a.n_shared = (int32_t)n_shared;
+    a.n_dense_rows = (int32_t)p.n_dense_rows;
+    a.dense_row_blocks = (int32_t)p.dense_row_blocks;
+    a.n_chunks = (int32_t)p.n_chunks;
+    a.chunk_keys = (int32_t)p.chunk_keys;
+    a.sparse_blocks = (int32_t)p.sparse_blocks;
+    a.items_per_bh = (int32_t)p.items_per_bh;
+    a.total_items = (int32_t)p.total_items;
+    a.n_bh = (int32_t)bh;
+    a.sparse = sparse ? 1 : 0;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    rc = hip_status(hilberta::launch_attn(a, dtype, (int)head_dim, s), "attention launch");
+    if (rc || p.n_chunks == 1) return rc;
+    hilberta::MergeArgs m{};
+    m.o = o;
+    m.lse = lse;
+    m.ws = a.ws;
+    m.sched = sched;
+    m.o_sb = os[0]; m.o_sh = os[1]; m.o_sr = os[2];
+    m.heads = (int32_t)heads;
+    m.n_tot = (int32_t)n_tot;
+    m.n_txt = (int32_t)n_txt;
+    m.span_cap = (int32_t)cap;
+    m.n_dense_rows = (int32_t)p.n_dense_rows;
+    m.n_chunks = (int32_t)p.n_chunks;
+    m.n_bh = (int32_t)bh;
+    m.n_tiles = (int32_t)n_tiles;
+    m.sparse = a.sparse;
+    return hip_status(hilberta::launch_merge(m, dtype, (int)head_dim, s), "merge launch");
+}
+
+int run_permute(bool scatter, const void* x, void* y, const int32_t* perm, int64_t batch, int64_t n,
+                int64_t channels, int64_t xbs, int64_t xrs, int64_t ybs, int64_t yrs, int dtype,
+                void* stream) {
+    if (!x || !y || !perm) return fail(HILBERTA_EINVAL, "NULL pointer");
+    if (batch < 0 || n < 0 || channels < 0) return fail(HILBERTA_EINVAL, "negative size");
+    if (n > 0x7fffffffLL) return fail(HILBERTA_EUNSUPPORTED, "more than 2^31 rows");
+    if (dtype != HILBERTA_F32 && dtype != HILBERTA_BF16)
+        return fail(HILBERTA_EUNSUPPORTED, "dtype %d", dtype);
+    if (xrs < channels || yrs < channels || xbs < 0 || ybs < 0)
+        return fail(HILBERTA_EINVAL, "row stride smaller than the row");
+    const int64_t es = dtype == HILBERTA_F32 ? 4 : 2;
+    hilberta::PermuteArgs a{};
+    a.x = static_cast<const char*>(x);
+    a.y = static_cast<char*>(y);
+    a.perm = perm;
+    a.batch = batch;
+    a.n = n;
+    a.row_bytes = channels * es;
+    a.x_bs = xbs * es;
+    a.x_rs = xrs * es;
+    a.y_bs = ybs * es;
+    a.y_rs = yrs * es;
+    a.scatter = scatter ? 1 : 0;
+    if (batch == 0 || n == 0 || channels == 0) return HILBERTA_OK;
+    return hip_status(hilberta::launch_permute(a, static_cast<hipStream_t>(stream)), "permute launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+int hilberta_version(void) { return 100; }
+
+const char* hilberta_last_error(void) { return g_err.c_str(); }
+
+int hilberta_build_perm(int32_t grid_h, int32_t grid_w, int32_t* perm, int32_t* inv_or_null,
+                        void* stream) {
+    if (!perm) return fail(HILBERTA_EINVAL, "perm is NULL");
+    if (grid_h != grid_w || !pow2(grid_w) || grid_w < 2 || grid_w > 32768)
+        return fail(HILBERTA_EUNSUPPORTED, "grid %dx%d is not a square power of two in [2, 32768]",
+                    grid_h, grid_w);
+    return hip_status(hilberta::launch_build_perm(grid_w, perm, inv_or_null,
+                                                  static_cast<hipStream_t>(stream)),
+                      "build_perm launch");
+}
+
+int hilberta_permute(const void* x, void* y, const int32_t* perm, int64_t batch, int64_t n,
+                     int64_t channels, int64_t x_batch_stride, int64_t x_row_stride,
+                     int64_t y_batch_stride, int64_t y_row_stride, int dtype, void* stream) {
+    return run_permute(false, x, y, perm, batch, n, channels, x_batch_stride, x_row_stride,
+                       y_batch_stride, y_row_stride, dtype, stream);
+}
+
+int hilberta_unpermute(const void* x, void* y, const int32_t* perm, int64_t batch, int64_t n,
+                       int64_t channels, int64_t x_batch_stride, int64_t x_row_stride,
+                       int64_t y_batch_stride, int64_t y_row_stride, int dtype, void* stream) {
+    return run_permute(true, x, y, perm, batch, n, channels, x_batch_stride, x_row_stride,
+                       y_batch_stride, y_row_stride, dtype, stream);
+}
+
+int hilberta_schedule_words(const hilberta_config* cfg, int64_t* words) {
+    int rc = check_config(cfg);
+    if (rc) return rc;
+    if (!words) return fail(HILBERTA_EINVAL, "words is NULL");
+    *words = schedule_words(cfg);
+    return HILBERTA_OK;
+}
+
+int hilberta_schedule(const hilberta_config* cfg, int32_t layer, int32_t* sched, int64_t capacity,
+                      int64_t* needed, void* stream) {
+    int rc = check_config(cfg);
+    if (rc) return rc;
+    if (layer < 0) return fail(HILBERTA_EINVAL, "layer %d < 0", layer);
+    const int64_t words = schedule_words(cfg);
+    if (needed) *needed = words;
+    if (!sched) return fail(HILBERTA_EINVAL, "sched is NULL");
+    if (capacity < words)
+        return fail(HILBERTA_ECAPACITY, "schedule needs %lld words, capacity %lld", (long long)words,
+                    (long long)capacity);
+    const int64_t n_img = (int64_t)cfg->grid_h * cfg->grid_w;
+    hilberta::ScheduleArgs a{};
+    a.out = sched;
+    a.grid_h = cfg->grid_h;
+    a.grid_w = cfg->grid_w;
+    a.n_txt = cfg->n_txt;
+    a.tile = cfg->tile;
+    a.n_tiles = (int32_t)(n_img / cfg->tile);
+    a.shared_h = cfg->shared_h;
+    a.shared_w = cfg->shared_w;
+    a.layer = layer;
+    a.offset = (int32_t)(((int64_t)layer * cfg->delta) % n_img);
+    a.span_cap = (int32_t)span_capacity(cfg);
+    a.words = (int32_t)words;
+    return hip_status(hilberta::launch_schedule(a, static_cast<hipStream_t>(stream)), "schedule launch");
+}
+
+int hilberta_attn_workspace_bytes(const hilberta_config* cfg, int64_t batch, int64_t heads,
+                                  int64_t head_dim, int dtype, int64_t* bytes) {
+    int rc = check_config(cfg);
+    if (rc) return rc;
+    if (!bytes) return fail(HILBERTA_EINVAL, "bytes is NULL");
+    if (batch < 0 || heads < 0) return fail(HILBERTA_EINVAL, "negative batch or heads");
+    if (head_dim != 64 && head_dim != 128)
+        return fail(HILBERTA_EUNSUPPORTED, "head_dim %lld not in {64, 128}", (long long)head_dim);
+    if (dtype != HILBERTA_F32 && dtype != HILBERTA_BF16) return fail(HILBERTA_EUNSUPPORTED, "dtype %d", dtype);
+    const int64_t n_img = (int64_t)cfg->grid_h * cfg->grid_w;
+    const int64_t n_tot = cfg->n_txt + n_img;
+    const Plan p = make_plan(true, cfg->n_txt, n_img, (int64_t)cfg->shared_h * cfg->shared_w,
+                             cfg->tile, n_tot, batch * heads, head_dim, true);
+    *bytes = p.ws_bytes;
+    return HILBERTA_OK;
+}
+
+int hilberta_attn_fwd(const hilberta_config* cfg, const int32_t* sched, const void* q, const void* k,
+                      const void* v, void* o, float* lse_or_null, int64_t batch, int64_t heads,
+                      int64_t head_dim, const int64_t q_strides[4], const int64_t k_strides[4],
+                      const int64_t v_strides[4], const int64_t o_strides[4], int dtype, float scale,
+                      void* workspace, int64_t workspace_bytes, void* stream) {
+    int rc = check_config(cfg);
+    if (rc) return rc;
+    if (!sched) return fail(HILBERTA_EINVAL, "sched is NULL");
+    const int64_t n_tot = cfg->n_txt + (int64_t)cfg->grid_h * cfg->grid_w;
+    return run_attention(true, cfg, sched, q, k, v, o, lse_or_null, batch, heads, n_tot, head_dim,
+                         q_strides, k_strides, v_strides, o_strides, dtype, scale, workspace,
+                         workspace_bytes, stream);
+}
+
+int dense_attn_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t head_dim, int dtype,
+                               int64_t* bytes) {
+    if (!bytes) return fail(HILBERTA_EINVAL, "bytes is NULL");
+    if (batch < 0 || heads < 0 || n < 0) return fail(HILBERTA_EINVAL, "negative size");
+    if (head_dim != 64 && head_dim != 128)
+        return fail(HILBERTA_EUNSUPPORTED, "head_dim %lld not in {64, 128}", (long long)head_dim);
+    if (dtype != HILBERTA_F32 && dtype != HILBERTA_BF16) return fail(HILBERTA_EUNSUPPORTED, "dtype %d", dtype);
+    const Plan p = make_plan(false, 0, n, 0, n, n, batch * heads, head_dim, true);
+    *bytes = p.ws_bytes;
+    return HILBERTA_OK;
+}
+
+int dense_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse_or_null,
+                   int64_t batch, int64_t heads, int64_t n, int64_t head_dim,
+                   const int64_t q_strides[4], const int64_t k_strides[4],
+                   const int64_t v_strides[4], const int64_t o_strides[4], int dtype, float scale,
+                   void* workspace, int64_t workspace_bytes, void* stream) {
+    if (n < 0) return fail(HILBERTA_EINVAL, "n < 0");
+    return run_attention(false, nullptr, nullptr, q, k, v, o, lse_or_null, batch, heads, n, head_dim,
+                         q_strides, k_strides, v_strides, o_strides, dtype, scale, workspace,
+                         workspace_bytes, stream);
+}
+
+}  // extern "C"

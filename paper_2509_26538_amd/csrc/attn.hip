@@ -1,0 +1,710 @@
+// HilbertA sparse attention forward and the dense baseline (§3.2-§3.4,
+// Appendix A, Algorithm 1), for gfx950.
+//
+// One launch covers every row of every (batch, head).  A workgroup of four
+// wavefronts owns a work item: 128 query rows and an ordered list of key
+// segments.  Keys stream through LDS in stages of 64 (double-buffered, the
+// next stage prefetched into registers while the current one is consumed).
+// Each wavefront owns 32 query rows and computes, per stage,
+//   S^T = K Q^T   with the MFMA (bf16: v_mfma_f32_32x32x16_bf16,
+//                 fp32: v_mfma_f32_32x32x2_f32),
+// so that every lane holds one query row and 32 of the 64 keys: the online
+// softmax (Algorithm 1's attn_inner: running max m, sum l, accumulator) is
+// per lane, with one cross-lane exchange for the row maximum.  Then
+//   O^T += V^T P^T,
+// where P^T is fed straight from the score registers.  The MFMA's reduction
+// index is free to enumerate the 16 keys of a chunk in any order, so V^T is
+// staged in LDS in exactly the key order the score registers hold; no
+// register shuffle of P is needed.
+//
+// Work items per (batch, head):
+//   dense items  -- rows that attend every key: the text and shared rows of
+//                   HilbertA (Appendix A treats both as a global prefix that
+//                   attends everything), or all rows of the dense baseline.
+//                   Their keys may be split into chunks whose partial
+//                   (acc, m, l) are merged by a second small kernel.
+//   sparse items -- 128 consecutive image rows.  Keys: the text span, the
+//                   shared tokens (gathered), and the slid tile(s) covering
+//                   the rows.  A tile that runs past the end of the image
+//                   span continues at its head (the modular indexing of
+//                   §3.2): two contiguous segments, addressed in place.
+// Each key is visited once: shared keys that also lie in the rows' tiles are
+// masked in the shared segment.  Rows of shared tokens inside a sparse item
+// are computed by the dense items and not stored here.
+#include "internal.hpp"
+
+#include <type_traits>
+
+namespace hilberta {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kKeyInvalid = -2;  // masked for every row
+constexpr int kKeyAll = -1;      // valid for every row
+enum : int32_t { SEG_CONTIG = 0, SEG_SHARED = 1, SEG_TILE = 2 };
+constexpr int kMaxSegs = 4;
+constexpr float kLn2 = 0.69314718055994530942f;
+
+struct Spans {
+    int32_t start[kMaxSpans];  // sequence position of the run's first token
+    int32_t len[kMaxSpans];
+    int32_t cum[kMaxSpans + 1];  // shared tokens before the run
+    int32_t n;
+};
+
+template <typename T, int D>
+struct Stage;
+
+template <int D>
+struct Stage<__bf16, D> {
+    uint16_t k[2][kBlockN][D + 8];    // K rows, padded against bank conflicts
+    uint16_t vt[2][D][kBlockN + 8];   // V^T in the key order of the P registers
+    int32_t info[2][kBlockN];
+};
+
+template <int D>
+struct Stage<float, D> {
+    float k[2][kBlockN][D + 1];
+    float v[2][kBlockN][D + 4];
+    int32_t info[2][kBlockN];
+};
+
+// Uniform (per-workgroup) description of one work item.
+struct Item {
+    int32_t bh;
+    int32_t dense;      // 1: dense item
+    int32_t chunk;      // dense: key chunk index
+    int32_t row0;       // dense: first dense row; sparse: first image position
+    int32_t o;          // slide offset of the layer
+    int32_t r_start;    // sparse: image position where the covering tiles begin
+    int32_t r_len;      //         and how many positions they cover
+    int32_t label_mask; // sparse: rows span more than one tile
+    int32_t nseg;
+    int32_t seg_base[kMaxSegs];
+    int32_t seg_len[kMaxSegs];
+    int32_t seg_kind[kMaxSegs];
+    int32_t nblk;
+};
+
+struct Block {
+    int32_t kind;
+    int32_t base;   // CONTIG/TILE: sequence position of the block's first key
+    int32_t first;  // SHARED: index of the block's first key among the shared tokens
+    int32_t cnt;    // keys present in the block (<= kBlockN)
+    bool fast;      // no per-key mask needed
+};
+
+__device__ inline int remap_xcd(int pid, int total) {
+    // Workgroups are dealt to the 8 XCDs round-robin; give each XCD one
+    // contiguous range of logical items so the items of a (batch, head),
+    // which share K and V, meet in one L2.
+    constexpr int X = 8;
+    const int per = (total + X - 1) / X;
+    int tall = total % X;
+    if (tall == 0) tall = X;
+    const int xcd = pid % X;
+    const int local = pid / X;
+    if (xcd < tall) return xcd * per + local;
+    return tall * per + (xcd - tall) * (per - 1) + local;
+}
+
+__device__ inline int32_t shared_seq(const Spans& sp, int32_t u) {
+    // sequence position of the u-th shared token (u < cum[n])
+    int32_t s = 0;
+    while (s + 1 < sp.n && u >= sp.cum[s + 1]) ++s;
+    return sp.start[s] + (u - sp.cum[s]);
+}
+
+__device__ inline bool is_shared_seq(const Spans& sp, int32_t seq) {
+    bool r = false;
+    for (int32_t s = 0; s < sp.n; ++s) r |= (seq >= sp.start[s]) & (seq < sp.start[s] + sp.len[s]);
+    return r;
+}
+
+__device__ inline int32_t tile_label(int32_t p, int32_t o, int32_t tile, int32_t n_img) {
+    return ((p + o) % n_img) / tile;
+}
+
+__device__ inline Block block_at(const Item& it, int32_t i) {
+    Block b{SEG_CONTIG, 0, 0, 0, false};
+    for (int s = 0; s < kMaxSegs; ++s) {
+        if (s >= it.nseg) break;
+        const int32_t nb = (it.seg_len[s] + kBlockN - 1) / kBlockN;
+        if (i < nb) {
+            b.kind = it.seg_kind[s];
+            b.first = i * kBlockN;
+            b.base = it.seg_base[s] + b.first;
+            b.cnt = min(kBlockN, it.seg_len[s] - b.first);
+            b.fast = b.cnt == kBlockN &&
+                     (b.kind == SEG_CONTIG || (b.kind == SEG_TILE && !it.label_mask));
+            return b;
+        }
+        i -= nb;
+    }
+    return b;
+}
+
+__device__ inline int32_t key_seq(const Block& b, int32_t r, const Spans& sp) {
+    const int32_t rr = r < b.cnt ? r : 0;  // absent keys read a present row
+    if (b.kind == SEG_SHARED) return shared_seq(sp, b.first + rr);
+    return b.base + rr;
+}
+
+__device__ inline int32_t key_info(const Block& b, int32_t r, int32_t seq, const Item& it,
+                                   const AttnArgs& a, const Spans& sp) {
+    if (r >= b.cnt) return kKeyInvalid;
+    if (b.kind == SEG_CONTIG) return kKeyAll;
+    const int32_t p = seq - a.n_txt;
+    if (b.kind == SEG_SHARED) {
+        const int32_t rel = (p - it.r_start + a.n_img) % a.n_img;
+        return rel < it.r_len ? kKeyInvalid : kKeyAll;  // counted in the tile segment
+    }
+    if (!it.label_mask || is_shared_seq(sp, seq)) return kKeyAll;
+    return tile_label(p, it.o, a.tile, a.n_img);
+}
+
+// ------------------------------------------------------------- staging
+template <typename T, int D>
+struct Loader;
+
+template <int D>
+struct Loader<__bf16, D> {
+    static constexpr int KCH = D / 8;                       // 16-byte chunks per K row
+    static constexpr int KPT = kBlockN * KCH / kThreads;    // per thread
+    static constexpr int VQ = D / 4;                        // 4-element quads per V row
+    static constexpr int VUNITS = 8 * VQ;                   // (8-key group, quad) units
+    uint4 kr[KPT];
+    uint2 vr[8];
+    int32_t info;
+
+    __device__ void load(const Block& b, const Item& it, const AttnArgs& a, const Spans& sp,
+                         const __bf16* kb, const __bf16* vb, int tid) {
+#pragma unroll
+        for (int j = 0; j < KPT; ++j) {
+            const int c = tid + kThreads * j;
+            const int row = c / KCH, col = c % KCH;
+            const int32_t seq = key_seq(b, row, sp);
+            kr[j] = *reinterpret_cast<const uint4*>(kb + (int64_t)seq * a.k_sr + col * 8);
+        }
+        if (tid < VUNITS) {
+            const int dq = tid % VQ, g = tid / VQ;
+            const int cc = g >> 1, hh = g & 1;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int krow = 16 * cc + 8 * (j >> 2) + 4 * hh + (j & 3);
+                const int32_t seq = key_seq(b, krow, sp);
+                vr[j] = *reinterpret_cast<const uint2*>(vb + (int64_t)seq * a.v_sr + 4 * dq);
+            }
+        }
+        if (tid < kBlockN) {
+            info = b.fast ? kKeyAll : key_info(b, tid, key_seq(b, tid, sp), it, a, sp);
+        }
+    }
+
+    __device__ void store(Stage<__bf16, D>& st, int buf, int tid) const {
+#pragma unroll
+        for (int j = 0; j < KPT; ++j) {
+            const int c = tid + kThreads * j;
+            const int row = c / KCH, col = c % KCH;
+            *reinterpret_cast<uint4*>(&st.k[buf][row][col * 8]) = kr[j];
+        }
+        if (tid < VUNITS) {
+            const int dq = tid % VQ, g = tid / VQ;
+            const int cc = g >> 1, hh = g & 1;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                // element e of each of the 8 keys, key j going to slot j
+                uint32_t w[4];
+#pragma unroll
+                for (int j = 0; j < 8; j += 2) {
+                    const uint32_t lo = (e < 2 ? vr[j].x : vr[j].y) >> (16 * (e & 1));
+                    const uint32_t hi = (e < 2 ? vr[j + 1].x : vr[j + 1].y) >> (16 * (e & 1));
+                    w[j >> 1] = (lo & 0xffffu) | (hi << 16);
+                }
+                *reinterpret_cast<uint4*>(&st.vt[buf][4 * dq + e][16 * cc + 8 * hh]) =
+                    make_uint4(w[0], w[1], w[2], w[3]);
+            }
+        }
+        if (tid < kBlockN) st.info[buf][tid] = info;
+    }
+};
+
+template <int D>
+struct Loader<float, D> {
+    static constexpr int CH = D / 4;                     // 16-byte chunks per row
+    static constexpr int PT = kBlockN * CH / kThreads;   // per thread, each of K and V
+    float4 kr[PT];
+    float4 vr[PT];
+    int32_t info;
+
+    __device__ void load(const Block& b, const Item& it, const AttnArgs& a, const Spans& sp,
+                         const float* kb, const float* vb, int tid) {
+#pragma unroll
+        for (int j = 0; j < PT; ++j) {
+            const int c = tid + kThreads * j;
+            const int row = c / CH, col = c % CH;
+            const int32_t seq = key_seq(b, row, sp);
+            kr[j] = *reinterpret_cast<const float4*>(kb + (int64_t)seq * a.k_sr + col * 4);
+            vr[j] = *reinterpret_cast<const float4*>(vb + (int64_t)seq * a.v_sr + col * 4);
+        }
+        if (tid < kBlockN) {
+            info = b.fast ? kKeyAll : key_info(b, tid, key_seq(b, tid, sp), it, a, sp);
+        }
+    }
+
+    __device__ void store(Stage<float, D>& st, int buf, int tid) const {
+#pragma unroll
+        for (int j = 0; j < PT; ++j) {
+            const int c = tid + kThreads * j;
+            const int row = c / CH, col = c % CH;
+            float* kd = &st.k[buf][row][col * 4];
+            kd[0] = kr[j].x;
+            kd[1] = kr[j].y;
+            kd[2] = kr[j].z;
+            kd[3] = kr[j].w;
+            *reinterpret_cast<float4*>(&st.v[buf][row][col * 4]) = vr[j];
+        }
+        if (tid < kBlockN) st.info[buf][tid] = info;
+    }
+};
+
+// ------------------------------------------------------------- Q operand
+template <typename T, int D>
+struct QOperand;
+
+template <int D>
+struct QOperand<__bf16, D> {
+    bf16x8 q[D / 16];  // Q[row][16 kc + 8 h .. + 8]
+    __device__ void load(const __bf16* qrow, int h) {
+#pragma unroll
+        for (int kc = 0; kc < D / 16; ++kc)
+            q[kc] = *reinterpret_cast<const bf16x8*>(qrow + 16 * kc + 8 * h);
+    }
+};
+
+template <int D>
+struct QOperand<float, D> {
+    float q[D / 2];  // Q[row][2 kc + h]
+    __device__ void load(const float* qrow, int h) {
+#pragma unroll
+        for (int kc = 0; kc < D / 2; ++kc) q[kc] = qrow[2 * kc + h];
+    }
+};
+
+// S^T for the 64 keys of a stage: s[kt] holds keys 32 kt + 8 (i/4) + 4 h + i%4
+// (register i) against the lane's query row.
+template <int D>
+__device__ inline void scores(const Stage<__bf16, D>& st, int buf, const QOperand<__bf16, D>& q,
+                              int ql, int h, f32x16 s[2]) {
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+        f32x16 acc = {};
+#pragma unroll
+        for (int kc = 0; kc < D / 16; ++kc) {
+            const bf16x8 a = *reinterpret_cast<const bf16x8*>(&st.k[buf][32 * kt + ql][16 * kc + 8 * h]);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, q.q[kc], acc, 0, 0, 0);
+        }
+        s[kt] = acc;
+    }
+}
+
+template <int D>
+__device__ inline void scores(const Stage<float, D>& st, int buf, const QOperand<float, D>& q,
+                              int ql, int h, f32x16 s[2]) {
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+        f32x16 acc = {};
+#pragma unroll
+        for (int kc = 0; kc < D / 2; ++kc) {
+            const float a = st.k[buf][32 * kt + ql][2 * kc + h];
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, q.q[kc], acc, 0, 0, 0);
+        }
+        s[kt] = acc;
+    }
+}
+
+// O^T += V^T P^T.  acc[dt] holds O^T rows d = 32 dt + 8 (i/4) + 4 h + i%4.
+template <int D>
+__device__ inline void accumulate(const Stage<__bf16, D>& st, int buf, const f32x16 p[2], int ql,
+                                  int h, f32x16 acc[D / 32]) {
+    bf16x8 pb[4];
+#pragma unroll
+    for (int cc = 0; cc < 4; ++cc) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) pb[cc][j] = (__bf16)p[cc >> 1][8 * (cc & 1) + j];
+    }
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) {
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) {
+            const bf16x8 a = *reinterpret_cast<const bf16x8*>(&st.vt[buf][32 * dt + ql][16 * cc + 8 * h]);
+            acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[cc], acc[dt], 0, 0, 0);
+        }
+    }
+}
+
+template <int D>
+__device__ inline void accumulate(const Stage<float, D>& st, int buf, const f32x16 p[2], int ql,
+                                  int h, f32x16 acc[D / 32]) {
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int key = 32 * kt + 8 * (i >> 2) + 4 * h + (i & 3);
+                const float a = st.v[buf][key][32 * dt + ql];
+                acc[dt] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, p[kt][i], acc[dt], 0, 0, 0);
+            }
+        }
+    }
+}
+
+template <typename T>
+__device__ inline void store4(T* dst, float a, float b, float c, float d);
+
+template <>
+__device__ inline void store4<__bf16>(__bf16* dst, float a, float b, float c, float d) {
+    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+    bf16x4 v = {(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
+    *reinterpret_cast<bf16x4*>(dst) = v;
+}
+
+template <>
+__device__ inline void store4<float>(float* dst, float a, float b, float c, float d) {
+    *reinterpret_cast<float4*>(dst) = make_float4(a, b, c, d);
+}
+
+// ------------------------------------------------------------- the kernel
+template <typename T, int D>
+struct Smem {
+    Stage<T, D> st;
+    Spans sp;
+};
+
+// bf16: two workgroups per CU (LDS and registers fit twice); fp32: one.
+template <typename T>
+struct Occupancy {
+    static constexpr int value = std::is_same<T, float>::value ? 1 : 2;
+};
+
+template <typename T, int D>
+__global__ void __launch_bounds__(kThreads, Occupancy<T>::value) attn_kernel(AttnArgs a) {
+    __shared__ Smem<T, D> sm;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int h = lane >> 5;
+    const int ql = lane & 31;
+
+    // ---- work item
+    const int item = remap_xcd(blockIdx.x, a.total_items);
+    Item it;
+    it.bh = item / a.items_per_bh;
+    int r = item - it.bh * a.items_per_bh;
+    const int dense_items = a.dense_row_blocks * a.n_chunks;
+    it.dense = r < dense_items;
+    it.o = 0;
+    it.r_start = 0;
+    it.r_len = 0;
+    it.label_mask = 0;
+    it.chunk = 0;
+
+    // ---- shared runs of the layer's table (HilbertA only)
+    if (a.sparse) {
+        const int32_t n_sp = min(max(a.sched[6], 0), min(a.span_cap, kMaxSpans));
+        const int32_t* tab = a.sched + 12 + 4 * a.n_tiles;
+        for (int s = tid; s < n_sp; s += kThreads) {
+            const int32_t st0 = min(max(tab[2 * s], a.n_txt), a.n_tot);
+            sm.sp.start[s] = st0;
+            sm.sp.len[s] = min(max(tab[2 * s + 1], 0), a.n_tot - st0);
+        }
+        __syncthreads();
+        if (tid == 0) {
+            int32_t c = 0;
+            for (int s = 0; s < n_sp; ++s) {
+                sm.sp.cum[s] = c;
+                c += sm.sp.len[s];
+            }
+            sm.sp.cum[n_sp] = c;
+            sm.sp.n = n_sp;
+        }
+        __syncthreads();
+        const int32_t o = a.sched[5];
+        it.o = ((o % a.n_img) + a.n_img) % a.n_img;
+    } else if (tid == 0) {
+        sm.sp.n = 0;
+        sm.sp.cum[0] = 0;
+    }
+    __syncthreads();
+    const int32_t n_shared = a.sparse ? sm.sp.cum[sm.sp.n] : 0;
+
+    // ---- this lane's query row
+    int32_t qseq = 0;       // sequence position of the row
+    bool row_ok = false;    // row exists
+    bool store_row = false; // this item writes the row
+    int32_t dense_row = -1; // dense items: row index among the dense rows
+    int32_t row_label = -3;
+    if (it.dense) {
+        const int rb = r / a.n_chunks;
+        it.chunk = r - rb * a.n_chunks;
+        it.row0 = rb * kBlockM;
+        dense_row = it.row0 + wave * 32 + ql;
+        if (dense_row < a.n_dense_rows) {
+            if (!a.sparse) {
+                qseq = dense_row;
+                row_ok = true;
+            } else if (dense_row < a.n_txt) {
+                qseq = dense_row;
+                row_ok = true;
+            } else if (dense_row - a.n_txt < n_shared) {
+                qseq = shared_seq(sm.sp, dense_row - a.n_txt);
+                row_ok = true;
+            }
+        }
+        store_row = row_ok;
+        const int32_t k0 = it.chunk * a.chunk_keys;
+        it.nseg = 1;
+        it.seg_base[0] = k0;
+        it.seg_len[0] = min(a.chunk_keys, a.n_tot - k0);
+        it.seg_kind[0] = SEG_CONTIG;
+    } else {
+        const int sb = r - dense_items;
+        it.row0 = sb * kBlockM;
+        const int32_t p = it.row0 + wave * 32 + ql;
+        const int32_t p_last = min(a.n_img, it.row0 + kBlockM) - 1;
+        row_ok = p < a.n_img;
+        const int32_t pc = row_ok ? p : p_last;
+        qseq = a.n_txt + pc;
+        store_row = row_ok && !is_shared_seq(sm.sp, qseq);
+        row_label = tile_label(pc, it.o, a.tile, a.n_img);
+        // tiles covering the rows: in the slid coordinate s = (p + o) mod N_img
+        // the rows are the cyclic run s0 .. s0 + L - 1, which meets the labels
+        // q1, q1 + 1, ... (mod T); a run as long as the image meets all T
+        const int32_t s0 = (it.row0 + it.o) % a.n_img;
+        const int32_t run = p_last - it.row0 + 1;
+        const int32_t q1 = s0 / a.tile;
+        const int32_t n_lab = min(a.n_tiles, (s0 + run - 1) / a.tile - q1 + 1);
+        it.label_mask = n_lab > 1;
+        it.r_start = (int32_t)(((int64_t)q1 * a.tile - it.o + a.n_img) % a.n_img);
+        it.r_len = min(n_lab * a.tile, a.n_img);
+        int ns = 0;
+        if (a.n_txt > 0) {
+            it.seg_base[ns] = 0;
+            it.seg_len[ns] = a.n_txt;
+            it.seg_kind[ns++] = SEG_CONTIG;
+        }
+        if (n_shared > 0) {
+            it.seg_base[ns] = 0;
+            it.seg_len[ns] = n_shared;
+            it.seg_kind[ns++] = SEG_SHARED;
+        }
+        const int32_t len_a = min(it.r_len, a.n_img - it.r_start);
+        it.seg_base[ns] = a.n_txt + it.r_start;
+        it.seg_len[ns] = len_a;
+        it.seg_kind[ns++] = SEG_TILE;
+        if (it.r_len > len_a) {
+            it.seg_base[ns] = a.n_txt;
+            it.seg_len[ns] = it.r_len - len_a;
+            it.seg_kind[ns++] = SEG_TILE;
+        }
+        it.nseg = ns;
+    }
+    it.nblk = 0;
+    for (int s = 0; s < it.nseg; ++s) it.nblk += (it.seg_len[s] + kBlockN - 1) / kBlockN;
+
+    const int32_t bb = it.bh / a.heads;
+    const int32_t hh = it.bh - bb * a.heads;
+    const T* qb = reinterpret_cast<const T*>(a.q) + bb * a.q_sb + hh * a.q_sh;
+    const T* kb = reinterpret_cast<const T*>(a.k) + bb * a.k_sb + hh * a.k_sh;
+    const T* vb = reinterpret_cast<const T*>(a.v) + bb * a.v_sb + hh * a.v_sh;
+
+    QOperand<T, D> qop;
+    qop.load(qb + (int64_t)qseq * a.q_sr, h);
+
+    f32x16 acc[D / 32];
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) acc[dt] = f32x16{};
+    float m_run = -INFINITY;  // running max of the scaled logits, log2 units
+    float l_run = 0.f;        // this lane's share of the running sum
+    const float c = a.scale_log2;
+
+    // ---- key stages
+    Loader<T, D> ld;
+    const int nblk = it.nblk;
+    if (nblk > 0) {
+        ld.load(block_at(it, 0), it, a, sm.sp, kb, vb, tid);
+        ld.store(sm.st, 0, tid);
+        if (nblk > 1) ld.load(block_at(it, 1), it, a, sm.sp, kb, vb, tid);
+    }
+    __syncthreads();
+    for (int i = 0; i < nblk; ++i) {
+        const int buf = i & 1;
+        const Block b = block_at(it, i);
+        f32x16 s[2];
+        scores<D>(sm.st, buf, qop, ql, h, s);
+        if (!b.fast) {
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int key = 32 * kt + 8 * (e >> 2) + 4 * h + (e & 3);
+                    const int32_t inf = sm.st.info[buf][key];
+                    const bool ok = inf == kKeyAll || inf == row_label;
+                    s[kt][e] = ok ? s[kt][e] : -INFINITY;
+                }
+            }
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt][e]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float m_new = fmaxf(m_run, mx * c);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+        m_run = m_new;
+        float lsum = 0.f;
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const float pe = __builtin_amdgcn_exp2f(fmaf(s[kt][e], c, -m_use));
+                s[kt][e] = pe;
+                lsum += pe;
+            }
+        l_run = l_run * alpha + lsum;
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) acc[dt] *= alpha;
+        accumulate<D>(sm.st, buf, s, ql, h, acc);
+
+        if (i + 1 < nblk) ld.store(sm.st, buf ^ 1, tid);
+        if (i + 2 < nblk) ld.load(block_at(it, i + 2), it, a, sm.sp, kb, vb, tid);
+        __syncthreads();
+    }
+
+    // ---- finalize
+    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    if (it.dense && a.n_chunks > 1) {
+        // partial (acc, m, l) of this key chunk, merged by merge_kernel
+        if (dense_row >= 0 && dense_row < a.n_dense_rows) {
+            const int64_t slot = ((int64_t)it.bh * a.n_chunks + it.chunk) * a.n_dense_rows + dense_row;
+            float* wacc = a.ws + slot * D;
+#pragma unroll
+            for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    *reinterpret_cast<float4*>(wacc + 32 * dt + 8 * g + 4 * h) =
+                        make_float4(acc[dt][4 * g], acc[dt][4 * g + 1], acc[dt][4 * g + 2],
+                                    acc[dt][4 * g + 3]);
+            if (h == 0) {
+                float* wml = a.ws + (int64_t)a.n_bh * a.n_chunks * a.n_dense_rows * D + slot * 2;
+                wml[0] = m_run;
+                wml[1] = l_tot;
+            }
+        }
+        return;
+    }
+    if (!store_row) return;
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    T* orow = reinterpret_cast<T*>(a.o) + bb * a.o_sb + hh * a.o_sh + (int64_t)qseq * a.o_sr;
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+            store4<T>(orow + 32 * dt + 8 * g + 4 * h, acc[dt][4 * g] * inv, acc[dt][4 * g + 1] * inv,
+                      acc[dt][4 * g + 2] * inv, acc[dt][4 * g + 3] * inv);
+    if (a.lse && h == 0) {
+        a.lse[(int64_t)it.bh * a.n_tot + qseq] =
+            l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
+    }
+}
+
+
+// Merge of the split key chunks of dense rows: with chunk partials
+// (acc_c, m_c, l_c), M = max m_c, L = sum l_c 2^(m_c - M) and
+// O = sum acc_c 2^(m_c - M) / L -- the same rescaling Algorithm 1 applies
+// between key blocks.  One wavefront per row.
+template <typename T, int D>
+__global__ void __launch_bounds__(256) merge_kernel(MergeArgs m) {
+    constexpr int EPL = D / 64;  // elements per lane
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int64_t rowid = (int64_t)blockIdx.x * 4 + wave;
+    if (rowid >= (int64_t)m.n_bh * m.n_dense_rows) return;
+    const int32_t bh = (int32_t)(rowid / m.n_dense_rows);
+    const int32_t r = (int32_t)(rowid - (int64_t)bh * m.n_dense_rows);
+    int32_t seq = r;
+    if (m.sparse && r >= m.n_txt) {
+        const int32_t n_sp = min(max(m.sched[6], 0), min(m.span_cap, kMaxSpans));
+        const int32_t* tab = m.sched + 12 + 4 * m.n_tiles;
+        int32_t u = r - m.n_txt;
+        seq = -1;
+        for (int32_t s = 0; s < n_sp; ++s) {
+            const int32_t st0 = min(max(tab[2 * s], m.n_txt), m.n_tot);
+            const int32_t ln = min(max(tab[2 * s + 1], 0), m.n_tot - st0);
+            if (u < ln) {
+                seq = st0 + u;
+                break;
+            }
+            u -= ln;
+        }
+        if (seq < 0) return;
+    }
+    const float* ml = m.ws + (int64_t)m.n_bh * m.n_chunks * m.n_dense_rows * D;
+    const int64_t slot0 = (int64_t)bh * m.n_chunks * m.n_dense_rows + r;
+    float mx = -INFINITY;
+    for (int c = 0; c < m.n_chunks; ++c) mx = fmaxf(mx, ml[(slot0 + (int64_t)c * m.n_dense_rows) * 2]);
+    const float m_use = mx == -INFINITY ? 0.f : mx;
+    float L = 0.f;
+    float o[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) o[e] = 0.f;
+    for (int c = 0; c < m.n_chunks; ++c) {
+        const int64_t slot = slot0 + (int64_t)c * m.n_dense_rows;
+        const float w = __builtin_amdgcn_exp2f(ml[slot * 2] - m_use);
+        L += w * ml[slot * 2 + 1];
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) o[e] += w * m.ws[slot * D + lane * EPL + e];
+    }
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    const int32_t b = bh / m.heads, hh = bh - b * m.heads;
+    T* orow = reinterpret_cast<T*>(m.o) + b * m.o_sb + hh * m.o_sh + (int64_t)seq * m.o_sr;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) orow[lane * EPL + e] = (T)(o[e] * inv);
+    if (m.lse && lane == 0)
+        m.lse[(int64_t)bh * m.n_tot + seq] = L > 0.f ? (m_use + log2f(L)) * kLn2 : -INFINITY;
+}
+
+template <typename T, int D>
+hipError_t launch_attn_t(const AttnArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL((attn_kernel<T, D>), dim3(a.total_items), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t launch_merge_t(const MergeArgs& m, hipStream_t s) {
+    const int64_t rows = (int64_t)m.n_bh * m.n_dense_rows;
+    const int64_t blocks = (rows + 3) / 4;
+    if (blocks == 0) return hipSuccess;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((merge_kernel<T, D>), dim3((unsigned)blocks), dim3(256), 0, s, m);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attn(const AttnArgs& a, int dtype, int head_dim, hipStream_t s) {
+    if (a.total_items == 0) return hipSuccess;
+    if (dtype == 1) return head_dim == 128 ? launch_attn_t<__bf16, 128>(a, s) : launch_attn_t<__bf16, 64>(a, s);
+    return head_dim == 128 ? launch_attn_t<float, 128>(a, s) : launch_attn_t<float, 64>(a, s);
+}
+
+hipError_t launch_merge(const MergeArgs& m, int dtype, int head_dim, hipStream_t s) {
+    if (dtype == 1) return head_dim == 128 ? launch_merge_t<__bf16, 128>(m, s) : launch_merge_t<__bf16, 64>(m, s);
+    return head_dim == 128 ? launch_merge_t<float, 128>(m, s) : launch_merge_t<float, 64>(m, s);
+}
+
+}  // namespace hilberta

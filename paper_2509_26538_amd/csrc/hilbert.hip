@@ -1,0 +1,199 @@
+// Hilbert linearisation (§3.1) and the per-layer schedule table (§3.2, §3.3).
+//
+// The Hilbert position d of a cell is decoded digit by digit: the base-4
+// digits of d, from the least significant, say which quadrant of the next
+// larger square the partial curve lies in and whether it is transposed
+// (and reflected) there.  Orientation: start (0, 0), end (side-1, 0),
+// x = column, y = row, raster index y*side + x.
+#include "internal.hpp"
+
+namespace hilberta {
+namespace {
+
+__device__ inline void hilbert_d2xy(int order, uint32_t d, uint32_t& x, uint32_t& y) {
+    uint32_t px = 0, py = 0;
+    for (int lvl = 0; lvl < order; ++lvl) {
+        const uint32_t s = 1u << lvl;
+        const uint32_t digit = (d >> (2 * lvl)) & 3u;
+        const uint32_t rx = digit >> 1;
+        const uint32_t ry = (digit ^ rx) & 1u;
+        if (ry == 0) {
+            if (rx) {
+                px = s - 1 - px;
+                py = s - 1 - py;
+            }
+            const uint32_t t = px;
+            px = py;
+            py = t;
+        }
+        px += s * rx;
+        py += s * ry;
+    }
+    x = px;
+    y = py;
+}
+
+// Inverse of hilbert_d2xy: peel the most significant quadrant first.
+__device__ inline uint32_t hilbert_xy2d(int order, uint32_t x, uint32_t y) {
+    uint32_t d = 0;
+    for (int lvl = order - 1; lvl >= 0; --lvl) {
+        const uint32_t s = 1u << lvl;
+        const uint32_t rx = (x >> lvl) & 1u;
+        const uint32_t ry = (y >> lvl) & 1u;
+        d += s * s * ((3u * rx) ^ ry);
+        x &= s - 1;
+        y &= s - 1;
+        if (ry == 0) {
+            const uint32_t t = x;
+            x = y;
+            y = t;
+            if (rx) {
+                x = s - 1 - x;
+                y = s - 1 - y;
+            }
+        }
+    }
+    return d;
+}
+
+__device__ inline int log2_side(int32_t side) { return 31 - __clz(side); }
+
+__global__ void __launch_bounds__(256) build_perm_kernel(int32_t side, int32_t* __restrict__ perm,
+                                                         int32_t* __restrict__ inv) {
+    const int order = log2_side(side);
+    const uint32_t n = (uint32_t)side * (uint32_t)side;
+    for (uint32_t d = blockIdx.x * blockDim.x + threadIdx.x; d < n; d += gridDim.x * blockDim.x) {
+        uint32_t x, y;
+        hilbert_d2xy(order, d, x, y);
+        const uint32_t raster = y * (uint32_t)side + x;
+        perm[d] = (int32_t)raster;
+        if (inv) inv[raster] = (int32_t)d;
+    }
+}
+
+// Shared runs: every cell of the central region finds its Hilbert position d
+// and whether it starts a run (d-1 lies outside the region, or d = 0) or ends
+// one (d+1 outside, or d = N-1).  Starts and ends are ranked separately; the
+// i-th start pairs with the i-th end.  One workgroup; also writes the header.
+__global__ void __launch_bounds__(256) shared_runs_kernel(ScheduleArgs a) {
+    __shared__ int32_t starts[kMaxSpans];
+    __shared__ int32_t ends[kMaxSpans];
+    __shared__ int32_t sorted_starts[kMaxSpans];
+    __shared__ int32_t sorted_ends[kMaxSpans];
+    __shared__ int32_t n_starts, n_ends;
+    const int tid = threadIdx.x;
+    const int order = log2_side(a.grid_w);
+    const uint32_t n_img = (uint32_t)a.grid_h * (uint32_t)a.grid_w;
+    const int32_t r0 = (a.grid_h - a.shared_h) / 2;
+    const int32_t c0 = (a.grid_w - a.shared_w) / 2;
+    const int32_t n_cells = a.shared_h * a.shared_w;
+    if (tid == 0) {
+        n_starts = 0;
+        n_ends = 0;
+    }
+    __syncthreads();
+    auto inside = [&](uint32_t d) {
+        uint32_t x, y;
+        hilbert_d2xy(order, d, x, y);
+        return (int32_t)y >= r0 && (int32_t)y < r0 + a.shared_h && (int32_t)x >= c0 &&
+               (int32_t)x < c0 + a.shared_w;
+    };
+    for (int32_t u = tid; u < n_cells; u += blockDim.x) {
+        const uint32_t y = (uint32_t)(r0 + u / a.shared_w);
+        const uint32_t x = (uint32_t)(c0 + u % a.shared_w);
+        const uint32_t d = hilbert_xy2d(order, x, y);
+        if (d == 0 || !inside(d - 1)) {
+            const int32_t i = atomicAdd(&n_starts, 1);
+            if (i < kMaxSpans) starts[i] = (int32_t)d;
+        }
+        if (d == n_img - 1 || !inside(d + 1)) {
+            const int32_t i = atomicAdd(&n_ends, 1);
+            if (i < kMaxSpans) ends[i] = (int32_t)d;
+        }
+    }
+    __syncthreads();
+    int32_t n_runs = min(min(n_starts, n_ends), a.span_cap);
+    n_runs = min(n_runs, kMaxSpans);
+    for (int32_t i = tid; i < n_runs; i += blockDim.x) {
+        int32_t rank_s = 0, rank_e = 0;
+        for (int32_t j = 0; j < n_runs; ++j) {
+            rank_s += starts[j] < starts[i];
+            rank_e += ends[j] < ends[i];
+        }
+        sorted_starts[rank_s] = starts[i];
+        sorted_ends[rank_e] = ends[i];
+    }
+    __syncthreads();
+    int32_t* spans = a.out + 12 + 4 * a.n_tiles;
+    for (int32_t i = tid; i < n_runs; i += blockDim.x) {
+        spans[2 * i] = a.n_txt + sorted_starts[i];
+        spans[2 * i + 1] = sorted_ends[i] + 1 - sorted_starts[i];
+    }
+    for (int32_t i = n_runs + tid; i < a.span_cap; i += blockDim.x) {
+        spans[2 * i] = 0;
+        spans[2 * i + 1] = 0;
+    }
+    if (tid == 0) {
+        int32_t* h = a.out;
+        h[0] = 0x48424131;
+        h[1] = a.n_txt;
+        h[2] = (int32_t)n_img;
+        h[3] = a.tile;
+        h[4] = a.n_tiles;
+        h[5] = a.offset;
+        h[6] = n_runs;
+        h[7] = n_cells;
+        h[8] = a.layer;
+        h[9] = a.grid_h;
+        h[10] = a.grid_w;
+        h[11] = a.span_cap;
+    }
+}
+
+// Tiles of the slid partition: tile q holds the image positions p with
+// floor(((p + o) mod N_img) / N_T) = q, i.e. the cyclic range that starts at
+// (q N_T - o) mod N_img.  Reads the runs written by shared_runs_kernel to
+// count the shared tokens inside each tile.
+__global__ void __launch_bounds__(256) tiles_kernel(ScheduleArgs a) {
+    const int32_t q = blockIdx.x * blockDim.x + threadIdx.x;
+    if (q >= a.n_tiles) return;
+    const int32_t n_img = a.grid_h * a.grid_w;
+    const int32_t start = (int32_t)(((int64_t)q * a.tile - a.offset + n_img) % n_img);
+    const int32_t len1 = min(a.tile, n_img - start);
+    const int32_t len2 = a.tile - len1;
+    const int32_t* spans = a.out + 12 + 4 * a.n_tiles;
+    const int32_t n_runs = a.out[6];
+    int32_t ns = 0;
+    for (int32_t s = 0; s < n_runs; ++s) {
+        const int32_t lo = spans[2 * s] - a.n_txt;
+        const int32_t hi = lo + spans[2 * s + 1];
+        ns += max(0, min(hi, start + len1) - max(lo, start));
+        ns += max(0, min(hi, len2) - max(lo, 0));
+    }
+    int32_t* t = a.out + 12 + 4 * q;
+    t[0] = a.n_txt + start;
+    t[1] = len1;
+    t[2] = len2;
+    t[3] = ns;
+}
+
+}  // namespace
+
+hipError_t launch_build_perm(int32_t side, int32_t* perm, int32_t* inv, hipStream_t s) {
+    const int64_t n = (int64_t)side * side;
+    const int64_t want = (n + 255) / 256;
+    const int blocks = (int)(want < 65536 ? want : 65536);
+    hipLaunchKernelGGL(build_perm_kernel, dim3(blocks), dim3(256), 0, s, side, perm, inv);
+    return hipGetLastError();
+}
+
+hipError_t launch_schedule(const ScheduleArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL(shared_runs_kernel, dim3(1), dim3(256), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int blocks = (a.n_tiles + 255) / 256;
+    hipLaunchKernelGGL(tiles_kernel, dim3(blocks), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace hilberta

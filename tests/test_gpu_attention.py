@@ -1,0 +1,130 @@
+"""GPU parity of hilberta_attn_fwd and dense_attn_fwd against the float64
+oracle: fp32 mode within 1e-5 max-abs, bf16 mode within 1e-2 max-abs and 1e-3
+mean-abs on the same bf16-rounded inputs.  Sizes span several query blocks
+(128 rows), several key stages (64 keys) and ragged tails."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle.schedule import Layout
+from paper_2509_26538_amd import synth
+
+from attn_util import (assert_close, hip_dense, hip_sparse, inputs, layout_of, oracle_rows,
+                       oracle_sparse)
+
+pytestmark = pytest.mark.gpu
+
+TINY = synth.WORKLOADS["tiny-16"]
+
+
+@pytest.mark.parametrize("layer", TINY.layers)
+@pytest.mark.parametrize("split", [False, True])
+def test_tiny_workload_fp32(gpu, layer, split):
+    layout = layout_of(TINY)
+    q, k, v = synth.qkv(TINY.batch, TINY.heads, TINY.n_tot, TINY.head_dim, "f32", seed=TINY.seed)
+    o, lse = hip_sparse(layout, layer, q, k, v, gpu, split=split)
+    ro, rl = oracle_sparse(layout, layer, q, k, v)
+    assert_close(o, ro, "f32", "O")
+    assert np.abs(lse - rl).max() <= 1e-5
+
+
+# Layouts that exercise every path: text, shared runs inside and outside the
+# covering tiles, the wrap tile, tiles shorter than a query block (per-row
+# tile masks), ragged text / shared / tile segments, one tile, no text.
+LAYOUTS = [
+    Layout(16, 16, 0, 64, 32, 4, 4),
+    Layout(16, 16, 77, 64, 40, 4, 4),
+    Layout(32, 32, 13, 256, 96, 8, 8),
+    Layout(32, 32, 130, 32, 24, 7, 5),
+    Layout(16, 16, 5, 256, 16, 0, 0),
+    Layout(8, 8, 3, 16, 5, 3, 2),
+    Layout(2, 2, 1, 1, 1, 1, 1),
+    Layout(4, 4, 0, 4, 3, 2, 2),
+]
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_layouts_fp32(gpu, layout, head_dim):
+    q, k, v = inputs(layout, 2, 2, head_dim, "f32", seed=layout.n_tot + head_dim)
+    for layer in (0, 1, 3):
+        o, lse = hip_sparse(layout, layer, q, k, v, gpu)
+        ro, rl = oracle_sparse(layout, layer, q, k, v)
+        assert_close(o, ro, "f32", "layer %d" % layer)
+        assert np.abs(lse - rl).max() <= 1e-5
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_layouts_bf16(gpu, layout, head_dim):
+    q, k, v = inputs(layout, 1, 3, head_dim, "bf16", seed=layout.n_tot + 2 * head_dim)
+    for layer in (0, 1, 2):
+        for split in (False, True):
+            o, lse = hip_sparse(layout, layer, q, k, v, gpu, split=split)
+            ro, rl = oracle_sparse(layout, layer, q, k, v)
+            assert_close(o, ro, "bf16", "layer %d split %s" % (layer, split))
+            assert np.abs(lse - rl).max() <= 1e-3
+
+
+def test_sharp_softmax_bf16(gpu):
+    # logits scaled up 4x: a missing or duplicated key shows up clearly
+    layout = Layout(32, 32, 40, 128, 64, 6, 6)
+    q, k, v = inputs(layout, 1, 2, 128, "bf16", seed=9)
+    q = (q.float() * 4).to(torch.bfloat16)
+    for layer in (0, 1):
+        o, _ = hip_sparse(layout, layer, q, k, v, gpu)
+        ro, _ = oracle_sparse(layout, layer, q, k, v)
+        assert_close(o, ro, "bf16", "layer %d" % layer)
+
+
+def test_one_tile_equals_dense(gpu):
+    # §3.2 with N_T = N_img: a single tile is dense attention
+    layout = Layout(32, 32, 21, 1024, 256, 6, 6)
+    q, k, v = inputs(layout, 1, 2, 128, "f32", seed=11)
+    o, _ = hip_sparse(layout, 1, q, k, v, gpu)
+    od, _ = hip_dense(q, k, v, gpu)
+    rows = np.arange(layout.n_tot)
+    ro, _ = oracle_rows(None, 0, q, k, v, rows)
+    assert_close(o, ro, "f32", "sparse")
+    assert_close(od, ro, "f32", "dense")
+
+
+@pytest.mark.parametrize("n,dtype,head_dim", [(300, "f32", 64), (1000, "bf16", 128), (64, "bf16", 64),
+                                              (129, "f32", 128), (4608, "bf16", 128)])
+def test_dense_matches_oracle(gpu, n, dtype, head_dim):
+    q, k, v = synth.qkv(1, 2, n, head_dim, dtype, seed=n)
+    for split in (False, True):
+        o, lse = hip_dense(q, k, v, gpu, split=split)
+        ro, rl = oracle_rows(None, 0, q, k, v, np.arange(n))
+        assert_close(o, ro, dtype, "split %s" % split)
+        assert np.abs(lse - rl).max() <= (1e-5 if dtype == "f32" else 1e-3)
+
+
+def test_batch_and_strided_layout(gpu):
+    # [B, N, H, D] storage (Flux's layout) passed as a strided [B, H, N, D] view
+    layout = Layout(16, 16, 33, 64, 32, 4, 4)
+    q, k, v = inputs(layout, 3, 2, 64, "bf16", seed=12)
+    o1, l1 = hip_sparse(layout, 1, q, k, v, gpu)
+    o2, l2 = hip_sparse(layout, 1, q, k, v, gpu, layout_bnhd=True)
+    ro, _ = oracle_sparse(layout, 1, q, k, v)
+    assert_close(o1, ro, "bf16")
+    assert np.array_equal(o1, o2) and np.array_equal(l1, l2)
+
+
+def test_deterministic(gpu):
+    layout = Layout(32, 32, 64, 256, 128, 8, 8)
+    q, k, v = inputs(layout, 1, 4, 128, "bf16", seed=13)
+    a = hip_sparse(layout, 1, q, k, v, gpu)
+    b = hip_sparse(layout, 1, q, k, v, gpu)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def test_empty_batch_is_a_no_op(gpu):
+    from paper_2509_26538_amd import hilberta as hb
+    from attn_util import make_schedule
+    layout = Layout(16, 16, 0, 64, 32, 4, 4)
+    cfg, sched = make_schedule(layout, 0, gpu)
+    q = torch.zeros(0, 2, layout.n_tot, 64, dtype=torch.bfloat16, device=gpu)
+    hb.hilberta_attn_fwd(cfg, sched, q, q, q, q.clone())
+    torch.cuda.synchronize()
