@@ -1,0 +1,293 @@
+#!/usr/bin/env python
+"""Benchmark of the HilbertA hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+
+Workload (synthetic, seeded, Flux.1-dev shapes; no weights or prompts are
+available): the 2048x2048 image shape -- a 128x128 latent grid (16384 image
+tokens) plus 512 text tokens, 24 heads, head dim 128, bf16; tiles of 1024
+tokens sliding by 512 per layer; a 16x16 central shared region; hidden states
+[1, 16384, 3072] for the token gather.
+
+One step is one pass of the whole hot path as one transformer forward uses
+it: the Hilbert permutation, the gather of the hidden states into Hilbert
+order, then for each of Flux.1-dev's 57 blocks the layer's schedule and the
+fused sparse attention, then the scatter back to raster order.  Inputs are
+resident in HBM before the timed region.  ``value`` is the visited FLOPs of
+the 57 attention calls (4 * D * B * H * nnz of the exact pattern) divided by
+the step time.
+
+Also reported, from the same process: per-call sparse and dense attention
+time at the 128^2 and 64^2 shapes, the speedup over the in-harness dense
+kernel, the gather's bandwidth, the roofline of the attention launch, and the
+oracle's rate on a bounded sample of the same workload.
+"""
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "sparse attn ms/call + visited TFLOP/s at 64² and 128² latent grids; vs dense"
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+N_LAYERS = 57              # Flux.1-dev: 19 double-stream + 38 single-stream blocks
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--calls", type=int, default=20, help="per-call timings of each kernel")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the HilbertA hot path here is built and timed on a "
+              "single MI355X (no sharding, no collectives); --gpus %d is not supported." % args.gpus)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2509_26538_amd import hilberta as hb
+    from paper_2509_26538_amd import synth
+
+    dev = torch.device("cuda:0")
+    hb.load()
+    torch.cuda.set_device(dev)
+
+    def tables(w):
+        cfg = hb.make_config(w.grid, w.n_txt, w.tile, w.delta, w.shared)
+        words = hb.hilberta_schedule_words(cfg)
+        return cfg, words
+
+    def nnz_from_table(w, tab):
+        # tab: host copy of the schedule table; tile entries carry the shared
+        # tokens inside each tile
+        n_glob = w.n_txt + w.shared * w.shared
+        total = n_glob * w.n_tot
+        T = int(tab[4])
+        for q in range(T):
+            ns = int(tab[12 + 4 * q + 3])
+            total += (w.tile - ns) * (n_glob + w.tile - ns)
+        return total
+
+    def setup(w):
+        cfg, words = tables(w)
+        q, k, v = synth.qkv(w.batch, w.heads, w.n_tot, w.head_dim, w.dtype, seed=w.seed)
+        q, k, v = q.to(dev), k.to(dev), v.to(dev)
+        o = torch.empty_like(q)
+        sched = torch.empty(words, dtype=torch.int32, device=dev)
+        ws_b = hb.hilberta_attn_workspace_bytes(cfg, w.batch, w.heads, w.head_dim, hb.HILBERTA_BF16)
+        ws = torch.empty(max(ws_b, 16), dtype=torch.uint8, device=dev)
+        dws_b = hb.dense_attn_workspace_bytes(w.batch, w.heads, w.n_tot, w.head_dim, hb.HILBERTA_BF16)
+        dws = torch.empty(max(dws_b, 16), dtype=torch.uint8, device=dev) if dws_b else None
+        return dict(cfg=cfg, q=q, k=k, v=v, o=o, sched=sched, ws=ws if ws_b else None, dws=dws)
+
+    def per_call(fn, n):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(n)]
+        for a, b in evs:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) for a, b in evs]
+
+    # ---------------------------------------------------------------- step
+    w = synth.WORKLOADS["flux-128"]
+    st = setup(w)
+    x = synth.hidden_states(1, w.n_img, w.hidden, "bf16", seed=1).to(dev)
+    y = torch.empty_like(x)
+    x_back = torch.empty_like(x)
+    perm = torch.empty(w.n_img, dtype=torch.int32, device=dev)
+
+    # visited FLOPs per layer from the schedule tables
+    layer_nnz = []
+    for layer in range(N_LAYERS):
+        hb.hilberta_schedule(st["cfg"], layer, st["sched"])
+        layer_nnz.append(nnz_from_table(w, st["sched"].cpu().numpy()))
+    flops_per_layer = [4 * w.head_dim * w.batch * w.heads * n for n in layer_nnz]
+    flops_per_step = sum(flops_per_layer)
+
+    attn_events = []
+
+    def step(record):
+        hb.hilberta_build_perm(w.grid, w.grid, perm)
+        hb.hilberta_permute(x, y, perm)
+        for layer in range(N_LAYERS):
+            hb.hilberta_schedule(st["cfg"], layer, st["sched"])
+            if record:
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+            hb.hilberta_attn_fwd(st["cfg"], st["sched"], st["q"], st["k"], st["v"], st["o"],
+                                 workspace=st["ws"])
+            if record:
+                b.record()
+                attn_events.append((layer, a, b))
+        hb.hilberta_unpermute(y, x_back, perm)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    t_start.record()
+    for _ in range(args.steps):
+        step(True)
+    t_end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+    value = flops_per_step / (ms_step * 1e-3) / 1e12
+    attn_ms = [a.elapsed_time(b) for _, a, b in attn_events]
+    attn_flops = [flops_per_layer[l] for l, _, _ in attn_events]
+    attn_avg_ms = statistics.fmean(attn_ms)
+    achieved = sum(attn_flops) / (sum(attn_ms) * 1e-3) / 1e12
+
+    # ------------------------------------------------------- per-call rows
+    def shape_report(wname, st_=None):
+        ww = synth.WORKLOADS[wname]
+        s = st_ or setup(ww)
+        hb.hilberta_schedule(s["cfg"], 1, s["sched"])
+        nnz1 = nnz_from_table(ww, s["sched"].cpu().numpy())
+        hb.hilberta_schedule(s["cfg"], 0, s["sched"])
+        nnz0 = nnz_from_table(ww, s["sched"].cpu().numpy())
+        sp = per_call(lambda: hb.hilberta_attn_fwd(s["cfg"], s["sched"], s["q"], s["k"], s["v"], s["o"],
+                                                   workspace=s["ws"]), args.calls)
+        de = per_call(lambda: hb.dense_attn_fwd(s["q"], s["k"], s["v"], s["o"], workspace=s["dws"]),
+                      args.calls)
+        sp_ms, de_ms = statistics.median(sp), statistics.median(de)
+        fl = 4 * ww.head_dim * ww.batch * ww.heads * nnz0
+        fl_dense = 4 * ww.head_dim * ww.batch * ww.heads * ww.n_tot ** 2
+        return {
+            "shape": "%dx%d latent + %d text, %d heads, D %d" % (ww.grid, ww.grid, ww.n_txt, ww.heads,
+                                                               ww.head_dim),
+            "sparse_ms_per_call": round(sp_ms, 4),
+            "sparse_visited_tflops": round(fl / (sp_ms * 1e-3) / 1e12, 1),
+            "sparse_gflop_per_call": round(fl / 1e9, 2),
+            "nnz_per_head_layer0_layer1": [nnz0, nnz1],
+            "dense_ms_per_call": round(de_ms, 4),
+            "dense_tflops": round(fl_dense / (de_ms * 1e-3) / 1e12, 1),
+            "speedup_vs_dense": round(de_ms / sp_ms, 2),
+        }
+
+    rep128 = shape_report("flux-128", st)
+    del st
+    torch.cuda.empty_cache()
+    rep64 = shape_report("flux-64")
+
+    # ------------------------------------------------------- token gather
+    flush = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device=dev)
+    gather_ms = []
+    for _ in range(args.calls):
+        flush.fill_(1)  # evict the 256 MB last-level cache
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        hb.hilberta_permute(x, y, perm)
+        b.record()
+        torch.cuda.synchronize()
+        gather_ms.append(a.elapsed_time(b))
+    del flush
+    gather_bytes = 2 * x.numel() * x.element_size() + perm.numel() * 4
+    gather_gbs = gather_bytes / (statistics.median(gather_ms) * 1e-3) / 1e9
+
+    # ------------------------------------------------------- HBM traffic
+    traffic = None
+    src = os.path.join(ROOT, "paper_2509_26538_amd", "csrc", "attn.hip")
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if os.path.exists(TRAFFIC_FILE):
+        rec = json.load(open(TRAFFIC_FILE))
+        if rec.get("attn_hip_sha256") == digest:
+            traffic = rec.get("bytes_per_launch")
+
+    # ------------------------------------------------------- CPU oracle
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w)
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) Q/K/V and hidden states of Flux.1-dev shapes)",
+        "config": {
+            "workload": "flux-128: 128x128 latent + 512 text tokens, 24 heads, D 128, tile 1024, "
+                        "slide 512/layer, shared 16x16; step = perm + gather + 57 x (schedule + "
+                        "sparse attention) + scatter",
+            "global_batch": w.batch,
+            "seq_len": w.n_tot,
+            "layers_per_step": N_LAYERS,
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(achieved, 1),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+            "kernel": "hilberta_attn_fwd (attn_kernel<bf16,128> + merge_kernel)",
+            "avg_launch_ms": round(attn_avg_ms, 4),
+            "flops_per_launch": round(statistics.fmean(attn_flops)),
+        },
+        "cpu_baseline": cpu,
+        "attn_128": rep128,
+        "attn_64": rep64,
+        "gather": {"bytes": gather_bytes, "ms_cold": round(statistics.median(gather_ms), 4),
+                   "GB/s": round(gather_gbs, 1), "frac_hbm": round(gather_gbs / PEAK_HBM_GBS, 3)},
+        "wall_s_timed": round(wall, 3),
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(w):
+    """The float64 oracle on a bounded sample of the workload's rows."""
+    import numpy as np
+    import torch
+
+    from oracle import attention, schedule
+    from oracle.schedule import Layout
+    from paper_2509_26538_amd import synth
+
+    layout = Layout(w.grid, w.grid, w.n_txt, w.tile, w.delta, w.shared, w.shared)
+    q, k, v = synth.qkv(w.batch, w.heads, w.n_tot, w.head_dim, w.dtype, seed=w.seed)
+    q64, k64, v64 = (t.to(torch.float64).numpy() for t in (q, k, v))
+    rows = np.arange(0, w.n_tot, w.n_tot // 64)[:64]
+    m = schedule.mask_rows(layout, 1, rows)
+    t0, c0 = time.perf_counter(), time.process_time()
+    attention.masked_attention_rows(q64, k64, v64, rows, m)
+    wall = time.perf_counter() - t0
+    cpu_s = time.process_time() - c0
+    flops = 4 * w.head_dim * w.batch * w.heads * int(m.sum())
+    return {
+        "value": flops / wall / 1e12,
+        "unit": "TFLOP/s",
+        "cores": max(1, round(cpu_s / wall)),
+        "kind": "oracle",
+        "sample": "%d query rows (every %d-th of %d, all 24 heads) of the 128x128 workload at "
+                  "layer 1; %.1f s wall, %.2f GFLOP visited" % (len(rows), w.n_tot // 64, w.n_tot,
+                                                                wall, flops / 1e9),
+        "host_cpus": os.cpu_count(),
+    }
+
+
+if __name__ == "__main__":
+    main()
