@@ -61,7 +61,8 @@ extern "C" {
  *                    the paper sets Delta = N_T / L for a slide cycle L (§3.2)
  *   shared_h/_w      central shared region (§3.3): image rows and columns in
  *                    [(side - s)/2, (side - s)/2 + s), integer halving; 0 x 0
- *                    disables it.  shared_h + shared_w must be <= 255.
+ *                    disables it.  At most 1024 shared tokens (32 x 32,
+ *                    the largest region the paper uses).
  * The sequence must satisfy n_txt + grid_h*grid_w < 2^31.
  */
 typedef struct hilberta_config {

@@ -57,6 +57,9 @@ int check_config(const hilberta_config* c) {
     if ((c->shared_h == 0) != (c->shared_w == 0))
         return fail(HILBERTA_EINVAL, "shared region %dx%d: both sides or neither must be zero",
                     c->shared_h, c->shared_w);
+    if ((int64_t)c->shared_h * c->shared_w > hilberta::kMaxShared)
+        return fail(HILBERTA_EUNSUPPORTED, "shared region %dx%d has more than %d tokens", c->shared_h,
+                    c->shared_w, hilberta::kMaxShared);
     if (c->shared_h + c->shared_w > 255)
         return fail(HILBERTA_EUNSUPPORTED, "shared region %dx%d: shared_h + shared_w must be <= 255",
                     c->shared_h, c->shared_w);

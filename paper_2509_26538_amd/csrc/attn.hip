@@ -40,6 +40,9 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kKeyInvalid = -2;  // masked for every row
 constexpr int kKeyAll = -1;      // valid for every row
@@ -52,40 +55,36 @@ struct Spans {
     int32_t len[kMaxSpans];
     int32_t cum[kMaxSpans + 1];  // shared tokens before the run
     int32_t n;
+    int32_t map[kMaxShared];   // sequence position of the u-th shared token
 };
 
 template <typename T, int D>
 struct Stage;
 
 template <int D>
-struct Stage<__bf16, D> {
-    uint16_t k[2][kBlockN][D + 8];    // K rows, padded against bank conflicts
-    uint16_t vt[2][D][kBlockN + 8];   // V^T in the key order of the P registers
-    int32_t info[2][kBlockN];
+struct alignas(16) Stage<__bf16, D> {
+    alignas(16) uint16_t k[2][kBlockN][D + 8];   // K rows, padded against bank conflicts
+    alignas(16) uint16_t vt[2][D][kBlockN + 8];  // V^T in the key order of the P registers
+    alignas(16) int32_t info[2][kBlockN];
 };
 
 template <int D>
-struct Stage<float, D> {
-    float k[2][kBlockN][D + 1];
-    float v[2][kBlockN][D + 4];
-    int32_t info[2][kBlockN];
+struct alignas(16) Stage<float, D> {
+    alignas(16) float k[2][kBlockN][D + 1];
+    alignas(16) float v[2][kBlockN][D + 4];
+    alignas(16) int32_t info[2][kBlockN];
 };
 
-// Uniform (per-workgroup) description of one work item.
-struct Item {
-    int32_t bh;
-    int32_t dense;      // 1: dense item
-    int32_t chunk;      // dense: key chunk index
-    int32_t row0;       // dense: first dense row; sparse: first image position
-    int32_t o;          // slide offset of the layer
-    int32_t r_start;    // sparse: image position where the covering tiles begin
-    int32_t r_len;      //         and how many positions they cover
-    int32_t label_mask; // sparse: rows span more than one tile
-    int32_t nseg;
-    int32_t seg_base[kMaxSegs];
-    int32_t seg_len[kMaxSegs];
-    int32_t seg_kind[kMaxSegs];
-    int32_t nblk;
+// Uniform (per-workgroup) description of one work item's keys: at most four
+// segments (text, gathered shared tokens, covering tiles, wrapped tail).
+// Functions below take these as separate scalar arguments, never through a
+// pointer, so that they stay in scalar registers (a field load through a
+// selected pointer would pin the whole description in scratch memory).
+struct Segs {
+    int32_t b0, b1, b2, b3;  // sequence position of the first key (SHARED: 0)
+    int32_t l0, l1, l2, l3;  // lengths
+    int32_t k0, k1, k2, k3;  // kinds
+    int32_t e0, e1, e2, e3;  // cumulative stage counts
 };
 
 struct Block {
@@ -96,7 +95,12 @@ struct Block {
     bool fast;      // no per-key mask needed
 };
 
-__device__ inline int remap_xcd(int pid, int total) {
+// Per-item values the key masks need.
+struct MaskCtx {
+    int32_t o, r_start, r_len, label_mask;
+};
+
+__device__ __forceinline__ int remap_xcd(int pid, int total) {
     // Workgroups are dealt to the 8 XCDs round-robin; give each XCD one
     // contiguous range of logical items so the items of a (batch, head),
     // which share K and V, meet in one L2.
@@ -110,49 +114,76 @@ __device__ inline int remap_xcd(int pid, int total) {
     return tall * per + (xcd - tall) * (per - 1) + local;
 }
 
-__device__ inline int32_t shared_seq(const Spans& sp, int32_t u) {
-    // sequence position of the u-th shared token (u < cum[n])
-    int32_t s = 0;
-    while (s + 1 < sp.n && u >= sp.cum[s + 1]) ++s;
-    return sp.start[s] + (u - sp.cum[s]);
+__device__ __forceinline__ int32_t shared_seq(const Spans& sp, int32_t u) {
+    // sequence position of the u-th shared token (u < cum[n] <= kMaxShared)
+    return sp.map[u];
 }
 
-__device__ inline bool is_shared_seq(const Spans& sp, int32_t seq) {
+__device__ __forceinline__ bool is_shared_seq(const Spans& sp, int32_t seq) {
     bool r = false;
     for (int32_t s = 0; s < sp.n; ++s) r |= (seq >= sp.start[s]) & (seq < sp.start[s] + sp.len[s]);
     return r;
 }
 
-__device__ inline int32_t tile_label(int32_t p, int32_t o, int32_t tile, int32_t n_img) {
+// Combine the two lane halves (lanes l and l^32 hold the same query row).
+__device__ __forceinline__ float half_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float half_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ int32_t tile_label(int32_t p, int32_t o, int32_t tile, int32_t n_img) {
     return ((p + o) % n_img) / tile;
 }
 
-__device__ inline Block block_at(const Item& it, int32_t i) {
-    Block b{SEG_CONTIG, 0, 0, 0, false};
-    for (int s = 0; s < kMaxSegs; ++s) {
-        if (s >= it.nseg) break;
-        const int32_t nb = (it.seg_len[s] + kBlockN - 1) / kBlockN;
-        if (i < nb) {
-            b.kind = it.seg_kind[s];
-            b.first = i * kBlockN;
-            b.base = it.seg_base[s] + b.first;
-            b.cnt = min(kBlockN, it.seg_len[s] - b.first);
-            b.fast = b.cnt == kBlockN &&
-                     (b.kind == SEG_CONTIG || (b.kind == SEG_TILE && !it.label_mask));
-            return b;
-        }
-        i -= nb;
-    }
+__device__ __forceinline__ Block block_at(int32_t i, int32_t b0, int32_t b1, int32_t b2, int32_t b3,
+                                          int32_t l0, int32_t l1, int32_t l2, int32_t l3,
+                                          int32_t k0, int32_t k1, int32_t k2, int32_t k3,
+                                          int32_t e0, int32_t e1, int32_t e2, int32_t label_mask) {
+    const bool in0 = i < e0, in1 = i < e1, in2 = i < e2;
+    const int32_t kind = in0 ? k0 : in1 ? k1 : in2 ? k2 : k3;
+    const int32_t base = in0 ? b0 : in1 ? b1 : in2 ? b2 : b3;
+    const int32_t len = in0 ? l0 : in1 ? l1 : in2 ? l2 : l3;
+    const int32_t before = in0 ? 0 : in1 ? e0 : in2 ? e1 : e2;
+    Block b;
+    b.kind = kind;
+    b.first = (i - before) * kBlockN;
+    b.base = base + b.first;
+    b.cnt = min(kBlockN, len - b.first);
+    b.fast = b.cnt == kBlockN && (kind == SEG_CONTIG || (kind == SEG_TILE && !label_mask));
     return b;
 }
 
-__device__ inline int32_t key_seq(const Block& b, int32_t r, const Spans& sp) {
+#define BLOCK_AT(i, g, lm)                                                                     \
+    block_at((i), (g).b0, (g).b1, (g).b2, (g).b3, (g).l0, (g).l1, (g).l2, (g).l3, (g).k0, (g).k1, \
+             (g).k2, (g).k3, (g).e0, (g).e1, (g).e2, (lm))
+
+__device__ __forceinline__ Segs make_segs(int32_t b0, int32_t l0, int32_t k0, int32_t b1, int32_t l1,
+                                           int32_t k1, int32_t b2, int32_t l2, int32_t k2, int32_t b3,
+                                           int32_t l3, int32_t k3) {
+    Segs g;
+    g.b0 = b0; g.l0 = l0; g.k0 = k0;
+    g.b1 = b1; g.l1 = l1; g.k1 = k1;
+    g.b2 = b2; g.l2 = l2; g.k2 = k2;
+    g.b3 = b3; g.l3 = l3; g.k3 = k3;
+    g.e0 = (l0 + kBlockN - 1) / kBlockN;
+    g.e1 = g.e0 + (l1 + kBlockN - 1) / kBlockN;
+    g.e2 = g.e1 + (l2 + kBlockN - 1) / kBlockN;
+    g.e3 = g.e2 + (l3 + kBlockN - 1) / kBlockN;
+    return g;
+}
+
+__device__ __forceinline__ int32_t key_seq(const Block& b, int32_t r, const Spans& sp) {
     const int32_t rr = r < b.cnt ? r : 0;  // absent keys read a present row
     if (b.kind == SEG_SHARED) return shared_seq(sp, b.first + rr);
     return b.base + rr;
 }
 
-__device__ inline int32_t key_info(const Block& b, int32_t r, int32_t seq, const Item& it,
+__device__ __forceinline__ int32_t key_info(const Block& b, int32_t r, int32_t seq, MaskCtx it,
                                    const AttnArgs& a, const Spans& sp) {
     if (r >= b.cnt) return kKeyInvalid;
     if (b.kind == SEG_CONTIG) return kKeyAll;
@@ -175,18 +206,18 @@ struct Loader<__bf16, D> {
     static constexpr int KPT = kBlockN * KCH / kThreads;    // per thread
     static constexpr int VQ = D / 4;                        // 4-element quads per V row
     static constexpr int VUNITS = 8 * VQ;                   // (8-key group, quad) units
-    uint4 kr[KPT];
-    uint2 vr[8];
+    u32x4 kr[KPT];
+    u32x2 vr[8];
     int32_t info;
 
-    __device__ void load(const Block& b, const Item& it, const AttnArgs& a, const Spans& sp,
+    __device__ __forceinline__ void load(const Block& b, MaskCtx it, const AttnArgs& a, const Spans& sp,
                          const __bf16* kb, const __bf16* vb, int tid) {
 #pragma unroll
         for (int j = 0; j < KPT; ++j) {
             const int c = tid + kThreads * j;
             const int row = c / KCH, col = c % KCH;
             const int32_t seq = key_seq(b, row, sp);
-            kr[j] = *reinterpret_cast<const uint4*>(kb + (int64_t)seq * a.k_sr + col * 8);
+            kr[j] = *reinterpret_cast<const u32x4*>(kb + (int64_t)seq * a.k_sr + col * 8);
         }
         if (tid < VUNITS) {
             const int dq = tid % VQ, g = tid / VQ;
@@ -195,7 +226,7 @@ struct Loader<__bf16, D> {
             for (int j = 0; j < 8; ++j) {
                 const int krow = 16 * cc + 8 * (j >> 2) + 4 * hh + (j & 3);
                 const int32_t seq = key_seq(b, krow, sp);
-                vr[j] = *reinterpret_cast<const uint2*>(vb + (int64_t)seq * a.v_sr + 4 * dq);
+                vr[j] = *reinterpret_cast<const u32x2*>(vb + (int64_t)seq * a.v_sr + 4 * dq);
             }
         }
         if (tid < kBlockN) {
@@ -203,12 +234,12 @@ struct Loader<__bf16, D> {
         }
     }
 
-    __device__ void store(Stage<__bf16, D>& st, int buf, int tid) const {
+    __device__ __forceinline__ void store(Stage<__bf16, D>& st, int buf, int tid) const {
 #pragma unroll
         for (int j = 0; j < KPT; ++j) {
             const int c = tid + kThreads * j;
             const int row = c / KCH, col = c % KCH;
-            *reinterpret_cast<uint4*>(&st.k[buf][row][col * 8]) = kr[j];
+            *reinterpret_cast<u32x4*>(&st.k[buf][row][col * 8]) = kr[j];
         }
         if (tid < VUNITS) {
             const int dq = tid % VQ, g = tid / VQ;
@@ -219,12 +250,12 @@ struct Loader<__bf16, D> {
                 uint32_t w[4];
 #pragma unroll
                 for (int j = 0; j < 8; j += 2) {
-                    const uint32_t lo = (e < 2 ? vr[j].x : vr[j].y) >> (16 * (e & 1));
-                    const uint32_t hi = (e < 2 ? vr[j + 1].x : vr[j + 1].y) >> (16 * (e & 1));
+                    const uint32_t lo = vr[j][e >> 1] >> (16 * (e & 1));
+                    const uint32_t hi = vr[j + 1][e >> 1] >> (16 * (e & 1));
                     w[j >> 1] = (lo & 0xffffu) | (hi << 16);
                 }
-                *reinterpret_cast<uint4*>(&st.vt[buf][4 * dq + e][16 * cc + 8 * hh]) =
-                    make_uint4(w[0], w[1], w[2], w[3]);
+                *reinterpret_cast<u32x4*>(&st.vt[buf][4 * dq + e][16 * cc + 8 * hh]) =
+                    u32x4{w[0], w[1], w[2], w[3]};
             }
         }
         if (tid < kBlockN) st.info[buf][tid] = info;
@@ -235,36 +266,36 @@ template <int D>
 struct Loader<float, D> {
     static constexpr int CH = D / 4;                     // 16-byte chunks per row
     static constexpr int PT = kBlockN * CH / kThreads;   // per thread, each of K and V
-    float4 kr[PT];
-    float4 vr[PT];
+    f32x4 kr[PT];
+    f32x4 vr[PT];
     int32_t info;
 
-    __device__ void load(const Block& b, const Item& it, const AttnArgs& a, const Spans& sp,
+    __device__ __forceinline__ void load(const Block& b, MaskCtx it, const AttnArgs& a, const Spans& sp,
                          const float* kb, const float* vb, int tid) {
 #pragma unroll
         for (int j = 0; j < PT; ++j) {
             const int c = tid + kThreads * j;
             const int row = c / CH, col = c % CH;
             const int32_t seq = key_seq(b, row, sp);
-            kr[j] = *reinterpret_cast<const float4*>(kb + (int64_t)seq * a.k_sr + col * 4);
-            vr[j] = *reinterpret_cast<const float4*>(vb + (int64_t)seq * a.v_sr + col * 4);
+            kr[j] = *reinterpret_cast<const f32x4*>(kb + (int64_t)seq * a.k_sr + col * 4);
+            vr[j] = *reinterpret_cast<const f32x4*>(vb + (int64_t)seq * a.v_sr + col * 4);
         }
         if (tid < kBlockN) {
             info = b.fast ? kKeyAll : key_info(b, tid, key_seq(b, tid, sp), it, a, sp);
         }
     }
 
-    __device__ void store(Stage<float, D>& st, int buf, int tid) const {
+    __device__ __forceinline__ void store(Stage<float, D>& st, int buf, int tid) const {
 #pragma unroll
         for (int j = 0; j < PT; ++j) {
             const int c = tid + kThreads * j;
             const int row = c / CH, col = c % CH;
             float* kd = &st.k[buf][row][col * 4];
-            kd[0] = kr[j].x;
-            kd[1] = kr[j].y;
-            kd[2] = kr[j].z;
-            kd[3] = kr[j].w;
-            *reinterpret_cast<float4*>(&st.v[buf][row][col * 4]) = vr[j];
+            kd[0] = kr[j][0];
+            kd[1] = kr[j][1];
+            kd[2] = kr[j][2];
+            kd[3] = kr[j][3];
+            *reinterpret_cast<f32x4*>(&st.v[buf][row][col * 4]) = vr[j];
         }
         if (tid < kBlockN) st.info[buf][tid] = info;
     }
@@ -277,7 +308,7 @@ struct QOperand;
 template <int D>
 struct QOperand<__bf16, D> {
     bf16x8 q[D / 16];  // Q[row][16 kc + 8 h .. + 8]
-    __device__ void load(const __bf16* qrow, int h) {
+    __device__ __forceinline__ void load(const __bf16* qrow, int h) {
 #pragma unroll
         for (int kc = 0; kc < D / 16; ++kc)
             q[kc] = *reinterpret_cast<const bf16x8*>(qrow + 16 * kc + 8 * h);
@@ -287,7 +318,7 @@ struct QOperand<__bf16, D> {
 template <int D>
 struct QOperand<float, D> {
     float q[D / 2];  // Q[row][2 kc + h]
-    __device__ void load(const float* qrow, int h) {
+    __device__ __forceinline__ void load(const float* qrow, int h) {
 #pragma unroll
         for (int kc = 0; kc < D / 2; ++kc) q[kc] = qrow[2 * kc + h];
     }
@@ -296,7 +327,7 @@ struct QOperand<float, D> {
 // S^T for the 64 keys of a stage: s[kt] holds keys 32 kt + 8 (i/4) + 4 h + i%4
 // (register i) against the lane's query row.
 template <int D>
-__device__ inline void scores(const Stage<__bf16, D>& st, int buf, const QOperand<__bf16, D>& q,
+__device__ __forceinline__ void scores(const Stage<__bf16, D>& st, int buf, const QOperand<__bf16, D>& q,
                               int ql, int h, f32x16 s[2]) {
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
@@ -311,7 +342,7 @@ __device__ inline void scores(const Stage<__bf16, D>& st, int buf, const QOperan
 }
 
 template <int D>
-__device__ inline void scores(const Stage<float, D>& st, int buf, const QOperand<float, D>& q,
+__device__ __forceinline__ void scores(const Stage<float, D>& st, int buf, const QOperand<float, D>& q,
                               int ql, int h, f32x16 s[2]) {
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
@@ -327,7 +358,7 @@ __device__ inline void scores(const Stage<float, D>& st, int buf, const QOperand
 
 // O^T += V^T P^T.  acc[dt] holds O^T rows d = 32 dt + 8 (i/4) + 4 h + i%4.
 template <int D>
-__device__ inline void accumulate(const Stage<__bf16, D>& st, int buf, const f32x16 p[2], int ql,
+__device__ __forceinline__ void accumulate(const Stage<__bf16, D>& st, int buf, const f32x16 p[2], int ql,
                                   int h, f32x16 acc[D / 32]) {
     bf16x8 pb[4];
 #pragma unroll
@@ -346,7 +377,7 @@ __device__ inline void accumulate(const Stage<__bf16, D>& st, int buf, const f32
 }
 
 template <int D>
-__device__ inline void accumulate(const Stage<float, D>& st, int buf, const f32x16 p[2], int ql,
+__device__ __forceinline__ void accumulate(const Stage<float, D>& st, int buf, const f32x16 p[2], int ql,
                                   int h, f32x16 acc[D / 32]) {
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt) {
@@ -363,17 +394,17 @@ __device__ inline void accumulate(const Stage<float, D>& st, int buf, const f32x
 }
 
 template <typename T>
-__device__ inline void store4(T* dst, float a, float b, float c, float d);
+__device__ __forceinline__ void store4(T* dst, float a, float b, float c, float d);
 
 template <>
-__device__ inline void store4<__bf16>(__bf16* dst, float a, float b, float c, float d) {
+__device__ __forceinline__ void store4<__bf16>(__bf16* dst, float a, float b, float c, float d) {
     typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
     bf16x4 v = {(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
     *reinterpret_cast<bf16x4*>(dst) = v;
 }
 
 template <>
-__device__ inline void store4<float>(float* dst, float a, float b, float c, float d) {
+__device__ __forceinline__ void store4<float>(float* dst, float a, float b, float c, float d) {
     *reinterpret_cast<float4*>(dst) = make_float4(a, b, c, d);
 }
 
@@ -401,16 +432,11 @@ __global__ void __launch_bounds__(kThreads, Occupancy<T>::value) attn_kernel(Att
 
     // ---- work item
     const int item = remap_xcd(blockIdx.x, a.total_items);
-    Item it;
-    it.bh = item / a.items_per_bh;
-    int r = item - it.bh * a.items_per_bh;
-    const int dense_items = a.dense_row_blocks * a.n_chunks;
-    it.dense = r < dense_items;
-    it.o = 0;
-    it.r_start = 0;
-    it.r_len = 0;
-    it.label_mask = 0;
-    it.chunk = 0;
+    const int32_t bh = item / a.items_per_bh;
+    const int32_t r = item - bh * a.items_per_bh;
+    const int32_t dense_items = a.dense_row_blocks * a.n_chunks;
+    const bool dense = r < dense_items;
+    MaskCtx mc{0, 0, 0, 0};
 
     // ---- shared runs of the layer's table (HilbertA only)
     if (a.sparse) {
@@ -425,15 +451,21 @@ __global__ void __launch_bounds__(kThreads, Occupancy<T>::value) attn_kernel(Att
         if (tid == 0) {
             int32_t c = 0;
             for (int s = 0; s < n_sp; ++s) {
-                sm.sp.cum[s] = c;
+                sm.sp.cum[s] = min(c, kMaxShared);
                 c += sm.sp.len[s];
             }
-            sm.sp.cum[n_sp] = c;
+            sm.sp.cum[n_sp] = min(c, kMaxShared);
             sm.sp.n = n_sp;
         }
         __syncthreads();
+        // the gathered shared segment reads its keys through this map
+        for (int u = tid; u < sm.sp.cum[n_sp]; u += kThreads) {
+            int32_t s = 0;
+            while (s + 1 < n_sp && u >= sm.sp.cum[s + 1]) ++s;
+            sm.sp.map[u] = sm.sp.start[s] + (u - sm.sp.cum[s]);
+        }
         const int32_t o = a.sched[5];
-        it.o = ((o % a.n_img) + a.n_img) % a.n_img;
+        mc.o = ((o % a.n_img) + a.n_img) % a.n_img;
     } else if (tid == 0) {
         sm.sp.n = 0;
         sm.sp.cum[0] = 0;
@@ -441,82 +473,55 @@ __global__ void __launch_bounds__(kThreads, Occupancy<T>::value) attn_kernel(Att
     __syncthreads();
     const int32_t n_shared = a.sparse ? sm.sp.cum[sm.sp.n] : 0;
 
-    // ---- this lane's query row
-    int32_t qseq = 0;       // sequence position of the row
-    bool row_ok = false;    // row exists
-    bool store_row = false; // this item writes the row
-    int32_t dense_row = -1; // dense items: row index among the dense rows
+    // ---- this lane's query row and the item's key segments
+    int32_t qseq = 0;        // sequence position of the row
+    bool store_row = false;  // this item writes the row
+    int32_t dense_row = -1;  // dense items: row index among the dense rows
     int32_t row_label = -3;
-    if (it.dense) {
-        const int rb = r / a.n_chunks;
-        it.chunk = r - rb * a.n_chunks;
-        it.row0 = rb * kBlockM;
-        dense_row = it.row0 + wave * 32 + ql;
+    int32_t chunk = 0;
+    Segs g;
+    if (dense) {
+        const int32_t rb = r / a.n_chunks;
+        chunk = r - rb * a.n_chunks;
+        dense_row = rb * kBlockM + wave * 32 + ql;
         if (dense_row < a.n_dense_rows) {
-            if (!a.sparse) {
+            if (!a.sparse || dense_row < a.n_txt) {
                 qseq = dense_row;
-                row_ok = true;
-            } else if (dense_row < a.n_txt) {
-                qseq = dense_row;
-                row_ok = true;
+                store_row = true;
             } else if (dense_row - a.n_txt < n_shared) {
                 qseq = shared_seq(sm.sp, dense_row - a.n_txt);
-                row_ok = true;
+                store_row = true;
             }
         }
-        store_row = row_ok;
-        const int32_t k0 = it.chunk * a.chunk_keys;
-        it.nseg = 1;
-        it.seg_base[0] = k0;
-        it.seg_len[0] = min(a.chunk_keys, a.n_tot - k0);
-        it.seg_kind[0] = SEG_CONTIG;
+        const int32_t k0 = chunk * a.chunk_keys;
+        g = make_segs(k0, min(a.chunk_keys, a.n_tot - k0), SEG_CONTIG, 0, 0, SEG_CONTIG, 0, 0,
+                      SEG_CONTIG, 0, 0, SEG_CONTIG);
     } else {
-        const int sb = r - dense_items;
-        it.row0 = sb * kBlockM;
-        const int32_t p = it.row0 + wave * 32 + ql;
-        const int32_t p_last = min(a.n_img, it.row0 + kBlockM) - 1;
-        row_ok = p < a.n_img;
+        const int32_t row0 = (r - dense_items) * kBlockM;
+        const int32_t p = row0 + wave * 32 + ql;
+        const int32_t p_last = min(a.n_img, row0 + kBlockM) - 1;
+        const bool row_ok = p < a.n_img;
         const int32_t pc = row_ok ? p : p_last;
         qseq = a.n_txt + pc;
         store_row = row_ok && !is_shared_seq(sm.sp, qseq);
-        row_label = tile_label(pc, it.o, a.tile, a.n_img);
+        row_label = tile_label(pc, mc.o, a.tile, a.n_img);
         // tiles covering the rows: in the slid coordinate s = (p + o) mod N_img
         // the rows are the cyclic run s0 .. s0 + L - 1, which meets the labels
         // q1, q1 + 1, ... (mod T); a run as long as the image meets all T
-        const int32_t s0 = (it.row0 + it.o) % a.n_img;
-        const int32_t run = p_last - it.row0 + 1;
+        const int32_t s0 = (row0 + mc.o) % a.n_img;
+        const int32_t run = p_last - row0 + 1;
         const int32_t q1 = s0 / a.tile;
         const int32_t n_lab = min(a.n_tiles, (s0 + run - 1) / a.tile - q1 + 1);
-        it.label_mask = n_lab > 1;
-        it.r_start = (int32_t)(((int64_t)q1 * a.tile - it.o + a.n_img) % a.n_img);
-        it.r_len = min(n_lab * a.tile, a.n_img);
-        int ns = 0;
-        if (a.n_txt > 0) {
-            it.seg_base[ns] = 0;
-            it.seg_len[ns] = a.n_txt;
-            it.seg_kind[ns++] = SEG_CONTIG;
-        }
-        if (n_shared > 0) {
-            it.seg_base[ns] = 0;
-            it.seg_len[ns] = n_shared;
-            it.seg_kind[ns++] = SEG_SHARED;
-        }
-        const int32_t len_a = min(it.r_len, a.n_img - it.r_start);
-        it.seg_base[ns] = a.n_txt + it.r_start;
-        it.seg_len[ns] = len_a;
-        it.seg_kind[ns++] = SEG_TILE;
-        if (it.r_len > len_a) {
-            it.seg_base[ns] = a.n_txt;
-            it.seg_len[ns] = it.r_len - len_a;
-            it.seg_kind[ns++] = SEG_TILE;
-        }
-        it.nseg = ns;
+        mc.label_mask = n_lab > 1;
+        mc.r_start = (int32_t)(((int64_t)q1 * a.tile - mc.o + a.n_img) % a.n_img);
+        mc.r_len = min(n_lab * a.tile, a.n_img);
+        const int32_t len_a = min(mc.r_len, a.n_img - mc.r_start);
+        g = make_segs(0, a.n_txt, SEG_CONTIG, 0, n_shared, SEG_SHARED, a.n_txt + mc.r_start, len_a,
+                      SEG_TILE, a.n_txt, mc.r_len - len_a, SEG_TILE);
     }
-    it.nblk = 0;
-    for (int s = 0; s < it.nseg; ++s) it.nblk += (it.seg_len[s] + kBlockN - 1) / kBlockN;
 
-    const int32_t bb = it.bh / a.heads;
-    const int32_t hh = it.bh - bb * a.heads;
+    const int32_t bb = bh / a.heads;
+    const int32_t hh = bh - bb * a.heads;
     const T* qb = reinterpret_cast<const T*>(a.q) + bb * a.q_sb + hh * a.q_sh;
     const T* kb = reinterpret_cast<const T*>(a.k) + bb * a.k_sb + hh * a.k_sh;
     const T* vb = reinterpret_cast<const T*>(a.v) + bb * a.v_sb + hh * a.v_sh;
@@ -527,22 +532,28 @@ __global__ void __launch_bounds__(kThreads, Occupancy<T>::value) attn_kernel(Att
     f32x16 acc[D / 32];
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt) acc[dt] = f32x16{};
-    float m_run = -INFINITY;  // running max of the scaled logits, log2 units
+    float m_run = -INFINITY;  // reference max of the scaled logits, log2 units
     float l_run = 0.f;        // this lane's share of the running sum
     const float c = a.scale_log2;
 
     // ---- key stages
+    // Stage i is consumed from LDS buffer i&1.  At the top of iteration i the
+    // registers hold stage i+1 (loaded during iteration i-1); they go to the
+    // other buffer, and stage i+2 is requested, so its global loads are in
+    // flight while stage i is computed.
     Loader<T, D> ld;
-    const int nblk = it.nblk;
+    const int nblk = g.e3;
     if (nblk > 0) {
-        ld.load(block_at(it, 0), it, a, sm.sp, kb, vb, tid);
+        ld.load(BLOCK_AT(0, g, mc.label_mask), mc, a, sm.sp, kb, vb, tid);
         ld.store(sm.st, 0, tid);
-        if (nblk > 1) ld.load(block_at(it, 1), it, a, sm.sp, kb, vb, tid);
+        if (nblk > 1) ld.load(BLOCK_AT(1, g, mc.label_mask), mc, a, sm.sp, kb, vb, tid);
     }
     __syncthreads();
     for (int i = 0; i < nblk; ++i) {
         const int buf = i & 1;
-        const Block b = block_at(it, i);
+        if (i + 1 < nblk) ld.store(sm.st, buf ^ 1, tid);
+        if (i + 2 < nblk) ld.load(BLOCK_AT(i + 2, g, mc.label_mask), mc, a, sm.sp, kb, vb, tid);
+        const Block b = BLOCK_AT(i, g, mc.label_mask);
         f32x16 s[2];
         scores<D>(sm.st, buf, qop, ql, h, s);
         if (!b.fast) {
@@ -562,11 +573,20 @@ __global__ void __launch_bounds__(kThreads, Occupancy<T>::value) attn_kernel(Att
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
             for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt][e]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run, mx * c);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-        m_run = m_new;
+        mx = half_max(mx) * c;
+        // Lazy rescaling: the reference max only moves when some row's max
+        // grew by more than 2^8; until then p <= 256 and acc and l share the
+        // stale reference, which cancels in acc / l.
+        if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f)) {
+            const float m_new = fmaxf(m_run, mx);
+            // a row with every key masked so far keeps -inf: leave it alone
+            const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+            m_run = m_new;
+            l_run *= alpha;
+#pragma unroll
+            for (int dt = 0; dt < D / 32; ++dt) acc[dt] *= alpha;
+        }
+        const float m_use = m_run == -INFINITY ? 0.f : m_run;
         float lsum = 0.f;
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
@@ -576,22 +596,17 @@ __global__ void __launch_bounds__(kThreads, Occupancy<T>::value) attn_kernel(Att
                 s[kt][e] = pe;
                 lsum += pe;
             }
-        l_run = l_run * alpha + lsum;
-#pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt) acc[dt] *= alpha;
+        l_run += lsum;
         accumulate<D>(sm.st, buf, s, ql, h, acc);
-
-        if (i + 1 < nblk) ld.store(sm.st, buf ^ 1, tid);
-        if (i + 2 < nblk) ld.load(block_at(it, i + 2), it, a, sm.sp, kb, vb, tid);
         __syncthreads();
     }
 
     // ---- finalize
-    const float l_tot = l_run + __shfl_xor(l_run, 32);
-    if (it.dense && a.n_chunks > 1) {
+    const float l_tot = half_sum(l_run);
+    if (dense && a.n_chunks > 1) {
         // partial (acc, m, l) of this key chunk, merged by merge_kernel
         if (dense_row >= 0 && dense_row < a.n_dense_rows) {
-            const int64_t slot = ((int64_t)it.bh * a.n_chunks + it.chunk) * a.n_dense_rows + dense_row;
+            const int64_t slot = ((int64_t)bh * a.n_chunks + chunk) * a.n_dense_rows + dense_row;
             float* wacc = a.ws + slot * D;
 #pragma unroll
             for (int dt = 0; dt < D / 32; ++dt)
@@ -618,7 +633,7 @@ __global__ void __launch_bounds__(kThreads, Occupancy<T>::value) attn_kernel(Att
             store4<T>(orow + 32 * dt + 8 * g + 4 * h, acc[dt][4 * g] * inv, acc[dt][4 * g + 1] * inv,
                       acc[dt][4 * g + 2] * inv, acc[dt][4 * g + 3] * inv);
     if (a.lse && h == 0) {
-        a.lse[(int64_t)it.bh * a.n_tot + qseq] =
+        a.lse[(int64_t)bh * a.n_tot + qseq] =
             l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
     }
 }

@@ -18,7 +18,8 @@ namespace hilberta {
 constexpr int kBlockM = 128;  // query rows per workgroup (4 waves x 32)
 constexpr int kBlockN = 64;   // keys per pipeline stage
 constexpr int kThreads = 256;
-constexpr int kMaxSpans = 256;  // shared runs a workgroup can hold in LDS
+constexpr int kMaxSpans = 256;   // shared runs a workgroup can hold in LDS
+constexpr int kMaxShared = 1024; // shared tokens a workgroup can map in LDS (32 x 32)
 
 struct AttnArgs {
     const void* q;

@@ -68,14 +68,18 @@ def test_layouts_bf16(gpu, layout, head_dim):
 
 
 def test_sharp_softmax_bf16(gpu):
-    # logits scaled up 4x: a missing or duplicated key shows up clearly
+    # Logits scaled up 4x, so a few keys dominate each row: a missing key
+    # moves an output by O(|v|) ~ 1 and a duplicated one by up to ~0.5.  The
+    # outputs then reach |O| ~ 4, where one bf16 ulp is 1.6e-2 and the
+    # dominant probability carries its own bf16 rounding, so the max-abs
+    # bound here is 2e-2 (mean-abs stays 1e-3).
     layout = Layout(32, 32, 40, 128, 64, 6, 6)
     q, k, v = inputs(layout, 1, 2, 128, "bf16", seed=9)
     q = (q.float() * 4).to(torch.bfloat16)
     for layer in (0, 1):
         o, _ = hip_sparse(layout, layer, q, k, v, gpu)
         ro, _ = oracle_sparse(layout, layer, q, k, v)
-        assert_close(o, ro, "bf16", "layer %d" % layer)
+        assert_close(o, ro, "bf16", "layer %d" % layer, max_abs=2e-2)
 
 
 def test_one_tile_equals_dense(gpu):
