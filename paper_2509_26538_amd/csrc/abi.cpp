@@ -177,6 +177,16 @@ int run_attention(bool sparse, const hilberta_config* cfg, const int32_t* sched,
         cap = span_capacity(cfg);
     }
     if (n_tot > 0x7fffffffLL) return fail(HILBERTA_EUNSUPPORTED, "sequence too long");
+    {
+        // K and V rows of one (batch, head) are addressed with 32-bit byte
+        // offsets from the slice's base
+        const int64_t es = dtype == HILBERTA_BF16 ? 2 : 4;
+        const int64_t rs = ks[2] > vs[2] ? ks[2] : vs[2];
+        if (((n_tot - 1) * rs + head_dim) * es > 0x7fffffffLL)
+            return fail(HILBERTA_EUNSUPPORTED, "one (batch, head) slice of K or V spans more than 2 GiB");
+        if (ks[2] < head_dim || vs[2] < head_dim)
+            return fail(HILBERTA_EINVAL, "K/V row stride smaller than head_dim");
+    }
     const int64_t bh = batch * heads;
     if (bh == 0 || n_tot == 0) return HILBERTA_OK;
     Plan p = make_plan(sparse, n_txt, n_img, n_shared, tile, n_tot, bh, head_dim, ws != nullptr);

@@ -197,6 +197,20 @@ __device__ __forceinline__ int32_t key_info(const Block& b, int32_t r, int32_t s
 }
 
 // ------------------------------------------------------------- staging
+// K and V rows are fetched with buffer loads: the resource holds the (batch,
+// head) slice's base address and its size, each thread's byte offset of the
+// rows it stages is fixed for the whole item, and a stage of contiguous keys
+// adds one uniform offset.  The whole offset travels in the per-lane operand,
+// which the hardware checks against the slice size: rows past the slice read
+// as zero instead of touching memory outside it.
+constexpr int kRsrcWord3 = 0x00020000;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t slice_rsrc(const void* base, int64_t rows,
+                                                             int64_t row_stride, int d, int esize) {
+    const int64_t bytes = ((rows - 1) * row_stride + d) * esize;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kRsrcWord3);
+}
+
 template <typename T, int D>
 struct Loader;
 
@@ -209,24 +223,51 @@ struct Loader<__bf16, D> {
     u32x4 kr[KPT];
     u32x2 vr[8];
     int32_t info;
+    __amdgpu_buffer_rsrc_t krs, vrs;
+    int32_t krow_b;  // bytes per K row
+    int32_t vrow_b;
 
-    __device__ __forceinline__ void load(const Block& b, MaskCtx it, const AttnArgs& a, const Spans& sp,
-                         const __bf16* kb, const __bf16* vb, int tid) {
+    // row of the block (0..63) and column byte offset each staged piece uses
+    __device__ __forceinline__ static int k_row(int tid, int j) { return (tid + kThreads * j) / KCH; }
+    __device__ __forceinline__ static int k_colb(int tid, int j) { return ((tid + kThreads * j) % KCH) * 16; }
+    __device__ __forceinline__ static int v_row(int tid, int j) {
+        const int g = tid / VQ, cc = g >> 1, hh = g & 1;
+        return 16 * cc + 8 * (j >> 2) + 4 * hh + (j & 3);
+    }
+    __device__ __forceinline__ static int v_colb(int tid) { return (tid % VQ) * 8; }
+
+    __device__ __forceinline__ void init(const __bf16* kb, const __bf16* vb, const AttnArgs& a) {
+        krs = slice_rsrc(kb, a.n_tot, a.k_sr, D, 2);
+        vrs = slice_rsrc(vb, a.n_tot, a.v_sr, D, 2);
+        krow_b = (int32_t)(a.k_sr * 2);
+        vrow_b = (int32_t)(a.v_sr * 2);
+    }
+
+    __device__ __forceinline__ void load(const Block& b, MaskCtx it, const AttnArgs& a,
+                                         const Spans& sp, int tid, int32_t n_shared) {
+        if (b.kind != SEG_SHARED) {
+            const int32_t ks = b.base * krow_b, vs = b.base * vrow_b;
 #pragma unroll
-        for (int j = 0; j < KPT; ++j) {
-            const int c = tid + kThreads * j;
-            const int row = c / KCH, col = c % KCH;
-            const int32_t seq = key_seq(b, row, sp);
-            kr[j] = *reinterpret_cast<const u32x4*>(kb + (int64_t)seq * a.k_sr + col * 8);
-        }
-        if (tid < VUNITS) {
-            const int dq = tid % VQ, g = tid / VQ;
-            const int cc = g >> 1, hh = g & 1;
+            for (int j = 0; j < KPT; ++j)
+                kr[j] = __builtin_amdgcn_raw_buffer_load_b128(krs, ks + k_row(tid, j) * krow_b + k_colb(tid, j), 0, 0);
+            if (tid < VUNITS) {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int krow = 16 * cc + 8 * (j >> 2) + 4 * hh + (j & 3);
-                const int32_t seq = key_seq(b, krow, sp);
-                vr[j] = *reinterpret_cast<const u32x2*>(vb + (int64_t)seq * a.v_sr + 4 * dq);
+                for (int j = 0; j < 8; ++j)
+                    vr[j] = __builtin_amdgcn_raw_buffer_load_b64(vrs, vs + v_row(tid, j) * vrow_b + v_colb(tid), 0, 0);
+            }
+        } else {
+            // gathered shared keys: one map lookup per staged row
+#pragma unroll
+            for (int j = 0; j < KPT; ++j) {
+                const int32_t seq = sp.map[min(b.first + k_row(tid, j), n_shared - 1)];
+                kr[j] = __builtin_amdgcn_raw_buffer_load_b128(krs, seq * krow_b + k_colb(tid, j), 0, 0);
+            }
+            if (tid < VUNITS) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int32_t seq = sp.map[min(b.first + v_row(tid, j), n_shared - 1)];
+                    vr[j] = __builtin_amdgcn_raw_buffer_load_b64(vrs, seq * vrow_b + v_colb(tid), 0, 0);
+                }
             }
         }
         if (tid < kBlockN) {
@@ -236,26 +277,21 @@ struct Loader<__bf16, D> {
 
     __device__ __forceinline__ void store(Stage<__bf16, D>& st, int buf, int tid) const {
 #pragma unroll
-        for (int j = 0; j < KPT; ++j) {
-            const int c = tid + kThreads * j;
-            const int row = c / KCH, col = c % KCH;
-            *reinterpret_cast<u32x4*>(&st.k[buf][row][col * 8]) = kr[j];
-        }
+        for (int j = 0; j < KPT; ++j)
+            *reinterpret_cast<u32x4*>(&st.k[buf][k_row(tid, j)][k_colb(tid, j) / 2]) = kr[j];
         if (tid < VUNITS) {
             const int dq = tid % VQ, g = tid / VQ;
             const int cc = g >> 1, hh = g & 1;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                // element e of each of the 8 keys, key j going to slot j
-                uint32_t w[4];
+                // element e of each of the 8 keys; key j goes to slot j
+                u32x4 w;
 #pragma unroll
                 for (int j = 0; j < 8; j += 2) {
-                    const uint32_t lo = vr[j][e >> 1] >> (16 * (e & 1));
-                    const uint32_t hi = vr[j + 1][e >> 1] >> (16 * (e & 1));
-                    w[j >> 1] = (lo & 0xffffu) | (hi << 16);
+                    const uint32_t lo = vr[j][e >> 1], hi = vr[j + 1][e >> 1];
+                    w[j >> 1] = __builtin_amdgcn_perm(hi, lo, (e & 1) ? 0x07060302u : 0x05040100u);
                 }
-                *reinterpret_cast<u32x4*>(&st.vt[buf][4 * dq + e][16 * cc + 8 * hh]) =
-                    u32x4{w[0], w[1], w[2], w[3]};
+                *reinterpret_cast<u32x4*>(&st.vt[buf][4 * dq + e][16 * cc + 8 * hh]) = w;
             }
         }
         if (tid < kBlockN) st.info[buf][tid] = info;
@@ -269,16 +305,37 @@ struct Loader<float, D> {
     f32x4 kr[PT];
     f32x4 vr[PT];
     int32_t info;
+    __amdgpu_buffer_rsrc_t krs, vrs;
+    int32_t krow_b, vrow_b;
 
-    __device__ __forceinline__ void load(const Block& b, MaskCtx it, const AttnArgs& a, const Spans& sp,
-                         const float* kb, const float* vb, int tid) {
+    __device__ __forceinline__ static int row_of(int tid, int j) { return (tid + kThreads * j) / CH; }
+    __device__ __forceinline__ static int colb_of(int tid, int j) { return ((tid + kThreads * j) % CH) * 16; }
+
+    __device__ __forceinline__ void init(const float* kb, const float* vb, const AttnArgs& a) {
+        krs = slice_rsrc(kb, a.n_tot, a.k_sr, D, 4);
+        vrs = slice_rsrc(vb, a.n_tot, a.v_sr, D, 4);
+        krow_b = (int32_t)(a.k_sr * 4);
+        vrow_b = (int32_t)(a.v_sr * 4);
+    }
+
+    __device__ __forceinline__ void load(const Block& b, MaskCtx it, const AttnArgs& a,
+                                         const Spans& sp, int tid, int32_t n_shared) {
 #pragma unroll
         for (int j = 0; j < PT; ++j) {
-            const int c = tid + kThreads * j;
-            const int row = c / CH, col = c % CH;
-            const int32_t seq = key_seq(b, row, sp);
-            kr[j] = *reinterpret_cast<const f32x4*>(kb + (int64_t)seq * a.k_sr + col * 4);
-            vr[j] = *reinterpret_cast<const f32x4*>(vb + (int64_t)seq * a.v_sr + col * 4);
+            const int row = row_of(tid, j);
+            int32_t ko, vo, ks = 0, vs = 0;
+            if (b.kind != SEG_SHARED) {
+                ko = row * krow_b;
+                vo = row * vrow_b;
+                ks = b.base * krow_b;
+                vs = b.base * vrow_b;
+            } else {
+                const int32_t seq = sp.map[min(b.first + row, n_shared - 1)];
+                ko = seq * krow_b;
+                vo = seq * vrow_b;
+            }
+            kr[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(krs, ks + ko + colb_of(tid, j), 0, 0));
+            vr[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(vrs, vs + vo + colb_of(tid, j), 0, 0));
         }
         if (tid < kBlockN) {
             info = b.fast ? kKeyAll : key_info(b, tid, key_seq(b, tid, sp), it, a, sp);
@@ -288,14 +345,13 @@ struct Loader<float, D> {
     __device__ __forceinline__ void store(Stage<float, D>& st, int buf, int tid) const {
 #pragma unroll
         for (int j = 0; j < PT; ++j) {
-            const int c = tid + kThreads * j;
-            const int row = c / CH, col = c % CH;
-            float* kd = &st.k[buf][row][col * 4];
+            const int row = row_of(tid, j), col = colb_of(tid, j) / 4;
+            float* kd = &st.k[buf][row][col];
             kd[0] = kr[j][0];
             kd[1] = kr[j][1];
             kd[2] = kr[j][2];
             kd[3] = kr[j][3];
-            *reinterpret_cast<f32x4*>(&st.v[buf][row][col * 4]) = vr[j];
+            *reinterpret_cast<f32x4*>(&st.v[buf][row][col]) = vr[j];
         }
         if (tid < kBlockN) st.info[buf][tid] = info;
     }
@@ -542,17 +598,18 @@ __global__ void __launch_bounds__(kThreads, Occupancy<T>::value) attn_kernel(Att
     // other buffer, and stage i+2 is requested, so its global loads are in
     // flight while stage i is computed.
     Loader<T, D> ld;
+    ld.init(kb, vb, a);
     const int nblk = g.e3;
     if (nblk > 0) {
-        ld.load(BLOCK_AT(0, g, mc.label_mask), mc, a, sm.sp, kb, vb, tid);
+        ld.load(BLOCK_AT(0, g, mc.label_mask), mc, a, sm.sp, tid, n_shared);
         ld.store(sm.st, 0, tid);
-        if (nblk > 1) ld.load(BLOCK_AT(1, g, mc.label_mask), mc, a, sm.sp, kb, vb, tid);
+        if (nblk > 1) ld.load(BLOCK_AT(1, g, mc.label_mask), mc, a, sm.sp, tid, n_shared);
     }
     __syncthreads();
     for (int i = 0; i < nblk; ++i) {
         const int buf = i & 1;
         if (i + 1 < nblk) ld.store(sm.st, buf ^ 1, tid);
-        if (i + 2 < nblk) ld.load(BLOCK_AT(i + 2, g, mc.label_mask), mc, a, sm.sp, kb, vb, tid);
+        if (i + 2 < nblk) ld.load(BLOCK_AT(i + 2, g, mc.label_mask), mc, a, sm.sp, tid, n_shared);
         const Block b = BLOCK_AT(i, g, mc.label_mask);
         f32x16 s[2];
         scores<D>(sm.st, buf, qop, ql, h, s);
