@@ -121,9 +121,10 @@ struct Plan {
 // list, so that no workgroup runs far longer than the rest; for the dense
 // baseline, split only when the rows alone would not fill the GPU a few times.
 Plan make_plan(bool sparse, int64_t n_txt, int64_t n_img, int64_t n_shared, int64_t tile,
-               int64_t n_tot, int64_t bh, int64_t head_dim, bool allow_split) {
+               int64_t n_tot, int64_t bh, int64_t head_dim, int dtype, bool allow_split) {
     Plan p{};
-    const int64_t bn = hilberta::kBlockN, bm = hilberta::kBlockM;
+    const int64_t bn = hilberta::kBlockN;
+    const int64_t bm = dtype == HILBERTA_BF16 ? hilberta::kBlockMBf16 : hilberta::kBlockM;
     int64_t chunk = round_up(n_tot, bn);
     if (sparse) {
         p.n_dense_rows = n_txt + n_shared;
@@ -189,7 +190,7 @@ int run_attention(bool sparse, const hilberta_config* cfg, const int32_t* sched,
     }
     const int64_t bh = batch * heads;
     if (bh == 0 || n_tot == 0) return HILBERTA_OK;
-    Plan p = make_plan(sparse, n_txt, n_img, n_shared, tile, n_tot, bh, head_dim, ws != nullptr);
+    Plan p = make_plan(sparse, n_txt, n_img, n_shared, tile, n_tot, bh, head_dim, dtype, ws != nullptr);
     if (ws && ws_bytes < p.ws_bytes)
         return fail(HILBERTA_ECAPACITY, "workspace of %lld bytes, %lld needed", (long long)ws_bytes,
                     (long long)p.ws_bytes);
@@ -354,7 +355,7 @@ int hilberta_attn_workspace_bytes(const hilberta_config* cfg, int64_t batch, int
     const int64_t n_img = (int64_t)cfg->grid_h * cfg->grid_w;
     const int64_t n_tot = cfg->n_txt + n_img;
     const Plan p = make_plan(true, cfg->n_txt, n_img, (int64_t)cfg->shared_h * cfg->shared_w,
-                             cfg->tile, n_tot, batch * heads, head_dim, true);
+                             cfg->tile, n_tot, batch * heads, head_dim, dtype, true);
     *bytes = p.ws_bytes;
     return HILBERTA_OK;
 }
@@ -380,7 +381,7 @@ int dense_attn_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t 
     if (head_dim != 64 && head_dim != 128)
         return fail(HILBERTA_EUNSUPPORTED, "head_dim %lld not in {64, 128}", (long long)head_dim);
     if (dtype != HILBERTA_F32 && dtype != HILBERTA_BF16) return fail(HILBERTA_EUNSUPPORTED, "dtype %d", dtype);
-    const Plan p = make_plan(false, 0, n, 0, n, n, batch * heads, head_dim, true);
+    const Plan p = make_plan(false, 0, n, 0, n, n, batch * heads, head_dim, dtype, true);
     *bytes = p.ws_bytes;
     return HILBERTA_OK;
 }

@@ -15,7 +15,8 @@ namespace hilberta {
 //   sparse items: sparse_blocks query blocks of image rows (HilbertA only).
 // Items of one (batch, head) are contiguous in the logical order, dense
 // first, and the logical order is spread over the XCDs in contiguous ranges.
-constexpr int kBlockM = 128;  // query rows per workgroup (4 waves x 32)
+constexpr int kBlockM = 128;  // query rows per workgroup, fp32 kernel (4 waves x 32)
+constexpr int kBlockMBf16 = 128;  // query rows per workgroup, bf16 kernel (4 waves x 32)
 constexpr int kBlockN = 64;   // keys per pipeline stage
 constexpr int kThreads = 256;
 constexpr int kMaxSpans = 256;   // shared runs a workgroup can hold in LDS
@@ -70,8 +71,9 @@ struct MergeArgs {
     int32_t sparse;
 };
 
-// Launchers (defined in attn.hip); return a hipError_t.
+// Launchers (attn.hip, attn_bf16.hip); return a hipError_t.
 hipError_t launch_attn(const AttnArgs& a, int dtype, int head_dim, hipStream_t s);
+hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& m, int dtype, int head_dim, hipStream_t s);
 
 // ----------------------------------------------------- permutation, schedule
