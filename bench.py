@@ -39,7 +39,7 @@ METRIC = "sparse attn ms/call + visited TFLOP/s at 64² and 128² latent grids; 
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 N_LAYERS = 57              # Flux.1-dev: 19 double-stream + 38 single-stream blocks
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hilberta_attn_fwd_flux128_traffic.json")
 # sources the bf16 attention kernel is compiled from; counters taken on an
 # older build of them are not reported
 ATTN_SOURCES = ("attn_bf16.hip", "attn_common.hpp", "internal.hpp")
@@ -279,7 +279,8 @@ def cpu_baseline(w):
     layout = Layout(w.grid, w.grid, w.n_txt, w.tile, w.delta, w.shared, w.shared)
     q, k, v = synth.qkv(w.batch, w.heads, w.n_tot, w.head_dim, w.dtype, seed=w.seed)
     q64, k64, v64 = (t.to(torch.float64).numpy() for t in (q, k, v))
-    rows = np.arange(0, w.n_tot, w.n_tot // 64)[:64]
+    n_rows = 320  # about 10 s of the oracle on one host core
+    rows = np.arange(0, w.n_tot, w.n_tot // n_rows)[:n_rows]
     m = schedule.mask_rows(layout, 1, rows)
     t0, c0 = time.perf_counter(), time.process_time()
     attention.masked_attention_rows(q64, k64, v64, rows, m)
@@ -291,9 +292,9 @@ def cpu_baseline(w):
         "unit": "TFLOP/s",
         "cores": max(1, round(cpu_s / wall)),
         "kind": "oracle",
-        "sample": "%d query rows (every %d-th of %d, all 24 heads) of the 128x128 workload at "
-                  "layer 1; %.1f s wall, %.2f GFLOP visited" % (len(rows), w.n_tot // 64, w.n_tot,
-                                                                wall, flops / 1e9),
+        "sample": "%d query rows (every %d-th of %d, all %d heads) of the 128x128 workload at "
+                  "layer 1; %.1f s wall, %.2f GFLOP visited" % (len(rows), w.n_tot // n_rows, w.n_tot,
+                                                                w.heads, wall, flops / 1e9),
         "host_cpus": os.cpu_count(),
     }
 

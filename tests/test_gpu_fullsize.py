@@ -1,0 +1,136 @@
+"""GPU parity at the full Flux.1-dev shapes, in the launch configuration the
+benchmark times (bf16, split-K workspace for the dense rows, no LSE output).
+
+The float64 oracle cannot afford every row of a 16896-token sequence for 24
+heads, so it checks sampled rows one by one: text rows, shared rows, the rows
+on both sides of every slid tile boundary near the sample, the wrap tile, the
+first and last image rows and seeded random rows, on three heads.  Every
+output element is also checked against properties that hold at any size: it
+is finite (the output starts as NaN, so an unwritten row fails) and it lies
+within the range of its V column (softmax weights are a convex combination).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import schedule
+from paper_2509_26538_amd import hilberta as hb
+from paper_2509_26538_amd import synth
+
+from attn_util import assert_close, layout_of, make_schedule, oracle_rows, workspace
+
+pytestmark = pytest.mark.gpu
+
+HEADS = (0, 13, 23)
+
+
+def sample_rows(layout, layer, n_random=16, seed=0):
+    is_global, lab = schedule.token_classes(layout, layer)
+    n_txt, n_tot = layout.n_txt, layout.n_tot
+    rows = set()
+    if n_txt:
+        rows.update((0, n_txt // 2, n_txt - 1))
+    shared = np.nonzero(is_global[n_txt:])[0] + n_txt
+    if shared.size:
+        rows.update((int(shared[0]), int(shared[shared.size // 2]), int(shared[-1])))
+    # tile boundaries: positions whose label differs from the previous one
+    img = lab[n_txt:]
+    edges = np.nonzero(img != np.roll(img, 1))[0] + n_txt
+    for e in edges[:4]:
+        rows.update((int(e) - 1, int(e)))
+    # the wrap tile holds both the last and the first image positions
+    rows.update((n_txt, n_txt + 1, n_tot - 2, n_tot - 1))
+    rng = np.random.default_rng(seed + layer)
+    rows.update(int(r) for r in rng.integers(n_txt, n_tot, n_random))
+    return np.array(sorted(r for r in rows if 0 <= r < n_tot), dtype=np.int64)
+
+
+class Resident:
+    """Q, K, V of a workload on the GPU with the schedule and workspace the
+    benchmark uses."""
+
+    def __init__(self, name, dev):
+        self.w = w = synth.WORKLOADS[name]
+        self.layout = layout_of(w)
+        self.q, self.k, self.v = synth.qkv(w.batch, w.heads, w.n_tot, w.head_dim, w.dtype, seed=w.seed)
+        self.dev = dev
+        self.qd, self.kd, self.vd = (t.to(dev) for t in (self.q, self.k, self.v))
+        self.o = torch.empty_like(self.qd)
+        cfg, _ = make_schedule(self.layout, 0, dev)
+        ws_b = hb.hilberta_attn_workspace_bytes(cfg, w.batch, w.heads, w.head_dim, hb.HILBERTA_BF16)
+        self.ws = workspace(ws_b, dev)
+        # range of every V column, per (batch, head)
+        self.vmin = self.vd.float().amin(dim=2, keepdim=True)
+        self.vmax = self.vd.float().amax(dim=2, keepdim=True)
+
+    def run(self, layer, lse=None):
+        cfg, sched = make_schedule(self.layout, layer, self.dev)
+        self.o.fill_(float("nan"))
+        hb.hilberta_attn_fwd(cfg, sched, self.qd, self.kd, self.vd, self.o, lse, workspace=self.ws)
+        torch.cuda.synchronize()
+        return self.o
+
+    def check_all(self, o, what):
+        of = o.float()
+        assert bool(torch.isfinite(of).all()), "%s: non-finite outputs" % what
+        slack = 1e-2
+        assert bool((of >= self.vmin - slack).all()) and bool((of <= self.vmax + slack).all()), \
+            "%s: an output leaves its V column's range" % what
+
+    def check_rows(self, o, layer, rows, what):
+        hs = list(HEADS)
+        got = o[:, hs][:, :, rows].cpu().to(torch.float64).numpy()
+        ref, _ = oracle_rows(self.layout, layer, self.q[:, hs], self.k[:, hs], self.v[:, hs], rows)
+        assert_close(got, ref, "bf16", "%s rows %s" % (what, rows.tolist()[:8]))
+
+
+@pytest.fixture(scope="module")
+def flux128(gpu):
+    r = Resident("flux-128", gpu)
+    yield r
+    del r
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("layer", [0, 1, 2, 31, 56])
+def test_flux128_sampled_rows(flux128, layer):
+    o = flux128.run(layer)
+    flux128.check_all(o, "layer %d" % layer)
+    flux128.check_rows(o, layer, sample_rows(flux128.layout, layer), "layer %d" % layer)
+
+
+def test_flux128_lse_rows(flux128):
+    # the same launch with the log-sum-exp output requested
+    r = flux128
+    lse = torch.full(r.q.shape[:3], float("nan"), dtype=torch.float32, device=r.dev)
+    o = r.run(3, lse)
+    rows = sample_rows(r.layout, 3, n_random=8)
+    hs = list(HEADS)
+    _, rl = oracle_rows(r.layout, 3, r.q[:, hs], r.k[:, hs], r.v[:, hs], rows)
+    got = lse[:, hs][:, :, rows].cpu().to(torch.float64).numpy()
+    assert np.abs(got - rl).max() <= 1e-3
+    r.check_all(o, "layer 3")
+
+
+def test_flux64_layer_sweep(gpu):
+    # the slide offsets of all 57 transformer blocks of Flux.1-dev at
+    # 1024x1024, a few rows each
+    r = Resident("flux-64-sweep", gpu)
+    for layer in r.w.layers:
+        o = r.run(layer)
+        r.check_all(o, "layer %d" % layer)
+        rows = sample_rows(r.layout, layer, n_random=4, seed=100)
+        r.check_rows(o, layer, rows, "layer %d" % layer)
+
+
+def test_stress256_sampled_rows(gpu):
+    # 4096x4096 image: 65536 image tokens, tile 2048 and the largest shared
+    # region the library accepts (32 x 32 = 1024 tokens)
+    r = Resident("stress-256", gpu)
+    for layer in (1, 40):
+        o = r.run(layer)
+        r.check_all(o, "layer %d" % layer)
+        r.check_rows(o, layer, sample_rows(r.layout, layer, n_random=8), "layer %d" % layer)
+    del r
+    torch.cuda.empty_cache()
