@@ -102,7 +102,7 @@ def order_of(side):
 def build_perm(grid_h, grid_w):
     """perm[d] = raster index (y*W + x) of Hilbert position d, and its inverse.
 
-    Only square power-of-two grids have a Hilbert curve (§3.1; Appendix E
+    Only square power-of-two grids have a Hilbert curve (§3.1; Appendix D
     embeds other shapes in an enclosing grid, which this oracle does not do).
     """
     if grid_h != grid_w:
