@@ -3,128 +3,112 @@
 // bf16 for the PV product, bf16 output.
 //
 // A workgroup of four wavefronts owns 128 query rows (32 per wavefront); two
-// workgroups share a CU, so each SIMD interleaves two wavefronts.  Keys
-// stream through LDS in double-buffered stages of 64, the next stage staged
-// through registers with bounds-checked buffer loads while the current one
-// is consumed.  Per stage each wavefront computes
-//   S^T = K Q^T    on v_mfma_f32_32x32x16_bf16: every lane holds one query
-//                  row and 32 of the 64 keys, so the online softmax state
-//                  (Algorithm 1's attn_inner: max m, sum l, accumulator) is
-//                  per lane; the two lane halves meet through
-//                  v_permlane32_swap;
-//   O^T += V^T P^T with P^T straight from the score registers.  The MFMA
-//                  reduction index may enumerate the 16 keys of a chunk in
-//                  any order, so V^T is staged in LDS in exactly the key
-//                  order the score registers hold.
-// The reference max moves only when a row max grows by more than 2^8 (acc
-// and l share it, so it cancels in acc / l).
+// workgroups share a CU, so each SIMD interleaves two wavefronts.
+//
+// Keys.  An item's keys form one list visited in stages of 64: for a dense
+// item the contiguous keys of its chunk; for a sparse item the text keys,
+// then the shared tokens that lie outside the item's own tiles (compacted
+// once per item, so every shared key is valid for every row), then the
+// covering tiles' range and its wrapped tail (the modular indexing of §3.2,
+// two contiguous ranges addressed in place).  Only the list's last stage is
+// ragged, and per-row tile masks are needed only when the rows straddle two
+// tiles.
+//
+// Staging.  K and V rows go straight from global memory into LDS with
+// bounds-checked buffer_load ... lds (no staging registers), double
+// buffered: stage i+1 is requested when stage i starts.  Rows are stored
+// unpadded with their 16-byte chunks XOR-swizzled by row: K chunk c of row r
+// sits at c ^ (r mod 16), so the 16 lanes that read one 16-byte piece of 16
+// consecutive rows hit 16 different bank groups; V chunk c sits at
+// c ^ 4 (r mod 4), so the four rows that a transposing read touches at once
+// use disjoint 64-byte quarters of the banks.
+//
+// Per stage each wavefront computes
+//   S^T = K Q^T    on v_mfma_f32_32x32x16_bf16 with K as the A operand
+//                  (ds_read_b128) and Q in registers: each lane holds one
+//                  query row and 32 of the 64 keys, so the online softmax
+//                  state (Algorithm 1's attn_inner: max m, sum l,
+//                  accumulator) is per lane; the two lane halves meet
+//                  through v_permlane32_swap;
+//   O^T += V^T P^T with V^T assembled by two ds_read_b64_tr_b16 from the
+//                  row-major V rows, in exactly the key order the P
+//                  registers hold (the MFMA reduction index may enumerate a
+//                  chunk's keys in any order), and P^T straight from the
+//                  score registers.
+// All K operands of a stage are requested before its QK^T MFMAs and all V
+// operands before its softmax, so the LDS latency overlaps the matrix work.
+// The running sum is kept in fp32 as four independent partial sums.  The
+// reference max moves only when a row max grows by more than 2^8 (acc and l
+// share it, so it cancels in acc / l).
 #include "attn_common.hpp"
 
 namespace hilberta {
 namespace {
 
-constexpr int kBN2 = 64;  // keys per stage
+constexpr int kBN = 64;  // keys per stage
 static_assert(kBlockMBf16 == 128, "four wavefronts of 32 rows");
 
 template <int D>
-struct alignas(16) Stage2 {
-    alignas(16) uint16_t k[2][kBN2][D + 8];   // K rows (pitch an odd multiple of 16 B)
-    alignas(16) uint16_t vt[2][D][kBN2 + 8];  // V^T, keys in score-register order
-    alignas(16) int32_t info[2][kBN2];
+struct Geo {
+    static constexpr int CPR = D / 8;              // 16-byte chunks per row
+    static constexpr int ROWB = D * 2;             // bytes per row
+    static constexpr int STAGEB = kBN * ROWB;      // bytes per tensor and stage
+    static constexpr int IPW = STAGEB / 1024 / 4;  // 1 KB direct loads per wavefront and tensor
+    // chunk swizzles (XOR on the 16-byte chunk index of a row)
+    __device__ __forceinline__ static int fk(int row) { return D == 128 ? (row & 15) : ((row >> 1) & 7); }
+    __device__ __forceinline__ static int fv(int row) { return D == 128 ? 4 * (row & 3) : 4 * ((row >> 1) & 1); }
 };
 
 template <int D>
-struct Smem2 {
-    Stage2<D> st;
+struct Smem {
+    alignas(16) uint8_t k[2][Geo<D>::STAGEB];
+    alignas(16) uint8_t v[2][Geo<D>::STAGEB];
+    alignas(16) int32_t info[2][kBN];
     Spans sp;
+    int32_t n_keep;
 };
 
-template <int D>
-struct Loader2 {
-    static constexpr int KCH = D / 8;                     // 16-byte chunks per K row
-    static constexpr int KPT = kBN2 * KCH / kThreads;     // K chunks per thread
-    static constexpr int VQ = D / 4;                      // 4-element quads per V row
-    static constexpr int VUNITS = 8 * VQ;                 // (8-key group, quad) pairs
-    u32x4 kr[KPT];
-    u32x2 vr[8];
-    int32_t info;
-    __amdgpu_buffer_rsrc_t krs, vrs;
-    int32_t krow_b, vrow_b;
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-    // K piece j: row (tid + 256 j) / KCH, chunk (tid + 256 j) % KCH.
-    __device__ __forceinline__ static int k_row(int tid, int j) { return (tid + kThreads * j) / KCH; }
-    __device__ __forceinline__ static int k_colb(int tid, int j) { return ((tid + kThreads * j) % KCH) * 16; }
-    // V group g = tid / VQ = 2 cc + hh covers keys 16 cc + 8 (j/4) + 4 hh +
-    // j%4 (j < 8), which land in the eight consecutive slots 16 cc + 8 hh + j;
-    // quad dq = tid % VQ.
-    __device__ __forceinline__ static int v_row(int tid, int j) {
-        const int g = tid / VQ, cc = g >> 1, hh = g & 1;
-        return 16 * cc + 8 * (j >> 2) + 4 * hh + (j & 3);
-    }
-    __device__ __forceinline__ static int v_colb(int tid) { return (tid % VQ) * 8; }
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
 
-    __device__ __forceinline__ void init(const __bf16* kb, const __bf16* vb, const AttnArgs& a) {
-        krs = slice_rsrc(kb, a.n_tot, a.k_sr, D, 2);
-        vrs = slice_rsrc(vb, a.n_tot, a.v_sr, D, 2);
-        krow_b = (int32_t)(a.k_sr * 2);
-        vrow_b = (int32_t)(a.v_sr * 2);
-    }
+// One 16-byte-per-lane buffer load straight into LDS at lds_base + 16 lane,
+// bounds-checked against the resource.  Inline assembly, so that the
+// compiler does not guard later LDS reads with a wait for it: the kernel
+// waits for each stage explicitly before the barrier that publishes it.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rsrc, uint32_t lds_base, int32_t voff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :
+                 : "s"(lds_base), "v"(voff), "s"(rsrc)
+                 : "memory", "m0");
+}
 
-    __device__ __forceinline__ void load(const Block& b, MaskCtx it, const AttnArgs& a,
-                                         const Spans& sp, int tid, int32_t n_shared) {
-        if (b.kind != SEG_SHARED) {
-            const int32_t ks = b.base * krow_b, vs = b.base * vrow_b;
-#pragma unroll
-            for (int j = 0; j < KPT; ++j)
-                kr[j] = __builtin_amdgcn_raw_buffer_load_b128(krs, ks + k_row(tid, j) * krow_b + k_colb(tid, j), 0, 0);
-            if (tid < VUNITS) {
-#pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    vr[j] = __builtin_amdgcn_raw_buffer_load_b64(vrs, vs + v_row(tid, j) * vrow_b + v_colb(tid), 0, 0);
-            }
-        } else {
-            // gathered shared keys: one map lookup per staged row
-#pragma unroll
-            for (int j = 0; j < KPT; ++j) {
-                const int32_t seq = sp.map[min(b.first + k_row(tid, j), n_shared - 1)];
-                kr[j] = __builtin_amdgcn_raw_buffer_load_b128(krs, seq * krow_b + k_colb(tid, j), 0, 0);
-            }
-            if (tid < VUNITS) {
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int32_t seq = sp.map[min(b.first + v_row(tid, j), n_shared - 1)];
-                    vr[j] = __builtin_amdgcn_raw_buffer_load_b64(vrs, seq * vrow_b + v_colb(tid), 0, 0);
-                }
-            }
-        }
-        if (tid < kBN2) info = b.fast ? kKeyAll : key_info(b, tid, key_seq(b, tid, sp), it, a, sp);
-    }
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void*)p);
+}
 
-    __device__ __forceinline__ void store(Stage2<D>& st, int buf, int tid) const {
-#pragma unroll
-        for (int j = 0; j < KPT; ++j)
-            *reinterpret_cast<u32x4*>(&st.k[buf][k_row(tid, j)][k_colb(tid, j) / 2]) = kr[j];
-        if (tid < VUNITS) {
-            const int dq = tid % VQ, g = tid / VQ;
-            const int cc = g >> 1, hh = g & 1;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                // element e of each of the 8 keys; key j goes to slot j
-                const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-                u32x4 w;
-#pragma unroll
-                for (int j = 0; j < 8; j += 2)
-                    w[j >> 1] = __builtin_amdgcn_perm(vr[j + 1][e >> 1], vr[j][e >> 1], sel);
-                *reinterpret_cast<u32x4*>(&st.vt[buf][4 * dq + e][16 * cc + 8 * hh]) = w;
-            }
-        }
-        if (tid < kBN2) st.info[buf][tid] = info;
-    }
-};
+// Sequence position of key v of the list (segment boundaries b1 <= b2 <= b3;
+// segment 0 starts at s0, the shared map covers [b1, b2), segment 2 starts
+// at sa and segment 3 at sb).
+__device__ __forceinline__ int32_t list_seq(int32_t v, int32_t b1, int32_t b2, int32_t b3, int32_t s0,
+                                            int32_t sa, int32_t sb, const Spans& sp) {
+    if (v < b1) return s0 + v;
+    if (v < b2) return sp.map[v - b1];
+    if (v < b3) return sa + (v - b2);
+    return sb + (v - b3);
+}
 
 template <int D>
 __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
-    __shared__ Smem2<D> sm;
+    using G = Geo<D>;
+    __shared__ Smem<D> sm;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -136,13 +120,65 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
     const int32_t r = item - bh * a.items_per_bh;
     const int32_t dense_items = a.dense_row_blocks * a.n_chunks;
     const bool dense = r < dense_items;
-    MaskCtx mc{0, 0, 0, 0};
-    mc.o = load_spans<kThreads>(a, sm.sp, tid);
+    const int32_t o = load_spans<kThreads>(a, sm.sp, tid);
     const int32_t n_shared = a.sparse ? sm.sp.cum[sm.sp.n] : 0;
     const int32_t chunk = dense ? r % a.n_chunks : 0;
     const int32_t row0 = dense ? (r / a.n_chunks) * kBlockMBf16 : (r - dense_items) * kBlockMBf16;
-    const Segs g = item_segments<kBN2>(a, dense, chunk, row0, kBlockMBf16, n_shared, mc);
-    const RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, mc.o, n_shared, sm.sp);
+
+    // ------------------------------------------------------------ key list
+    int32_t b1, b2, b3, total, s0, sa, sb;
+    bool label_mask = false;
+    if (dense) {
+        s0 = chunk * a.chunk_keys;
+        total = min(a.chunk_keys, a.n_tot - s0);
+        b1 = b2 = b3 = total;
+        sa = sb = 0;
+    } else {
+        // tiles covering the rows: in the slid coordinate t = (p + o) mod
+        // N_img the rows are a cyclic run from t0 that meets labels q1,
+        // q1 + 1, ... (mod T); a run as long as the image meets all T
+        const int32_t p_last = min(a.n_img, row0 + kBlockMBf16) - 1;
+        const int32_t t0 = (row0 + o) % a.n_img;
+        const int32_t q1 = t0 / a.tile;
+        const int32_t n_lab = min(a.n_tiles, (t0 + p_last - row0) / a.tile - q1 + 1);
+        label_mask = n_lab > 1;
+        const int32_t r_start = (int32_t)(((int64_t)q1 * a.tile - o + a.n_img) % a.n_img);
+        const int32_t r_len = min(n_lab * a.tile, a.n_img);
+        const int32_t len_a = min(r_len, a.n_img - r_start);
+        // keep the shared tokens outside [r_start, r_start + r_len) (cyclic):
+        // those inside are keys of the tile segment already.  One wavefront
+        // compacts the map in place, in order.
+        if (wave == 0) {
+            int32_t w = 0;
+            for (int32_t u0 = 0; u0 < n_shared; u0 += 64) {
+                const int32_t u = u0 + lane;
+                int32_t seq = 0;
+                bool keep = false;
+                if (u < n_shared) {
+                    seq = sm.sp.map[u];
+                    const int32_t rel = (seq - a.n_txt - r_start + a.n_img) % a.n_img;
+                    keep = rel >= r_len;
+                }
+                const uint64_t bal = __builtin_amdgcn_ballot_w64(keep);
+                const int32_t before = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+                if (keep) sm.sp.map[w + before] = seq;
+                w += __builtin_popcountll(bal);
+            }
+            if (lane == 0) sm.n_keep = w;
+        }
+        __syncthreads();
+        const int32_t n_keep = sm.n_keep;
+        s0 = 0;
+        b1 = a.n_txt;
+        b2 = b1 + n_keep;
+        b3 = b2 + len_a;
+        total = b2 + r_len;
+        sa = a.n_txt + r_start;
+        sb = a.n_txt;
+    }
+    const int nblk = (total + kBN - 1) / kBN;
+    const RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
 
     const int32_t bb = bh / a.heads;
     const int32_t hh = bh - bb * a.heads;
@@ -154,88 +190,189 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
     for (int kc = 0; kc < D / 16; ++kc) q[kc] = *reinterpret_cast<const bf16x8*>(qrow + 16 * kc + 8 * h);
 
+    // Direct loads: wavefront w issues IPW 1 KB loads per tensor and stage;
+    // lane l of load j fills LDS chunk p = (w IPW + j) 64 + l of the stage,
+    // i.e. row p / CPR, stored chunk p % CPR, which holds global chunk
+    // (p % CPR) ^ f(row) of that row.
+    const __amdgpu_buffer_rsrc_t krs = slice_rsrc(kbase, a.n_tot, a.k_sr, D, 2);
+    const __amdgpu_buffer_rsrc_t vrs = slice_rsrc(vbase, a.n_tot, a.v_sr, D, 2);
+    const int32_t krow_b = (int32_t)(a.k_sr * 2), vrow_b = (int32_t)(a.v_sr * 2);
+    int32_t srow[G::IPW], kcol[G::IPW], vcol[G::IPW], koff[G::IPW], voff[G::IPW];
+#pragma unroll
+    for (int j = 0; j < G::IPW; ++j) {
+        const int p = (wave * G::IPW + j) * 64 + lane;
+        srow[j] = p / G::CPR;
+        kcol[j] = ((p % G::CPR) ^ G::fk(srow[j])) * 16;
+        vcol[j] = ((p % G::CPR) ^ G::fv(srow[j])) * 16;
+        koff[j] = srow[j] * krow_b + kcol[j];  // byte offset within a full contiguous stage
+        voff[j] = srow[j] * vrow_b + vcol[j];
+    }
+    const uint32_t klds0 = lds_addr(&sm.k[0][wave * G::IPW * 1024]);
+    const uint32_t vlds0 = lds_addr(&sm.v[0][wave * G::IPW * 1024]);
+
+    // does stage i need per-key masks (ragged end, or per-row tile labels)?
+    auto stage_fast = [&](int32_t i) -> bool {
+        const int32_t v0 = i * kBN;
+        return total - v0 >= kBN && !(label_mask && v0 + kBN > b2);
+    };
+    auto load_stage = [&](int32_t i, int buf) {
+        const int32_t v0 = i * kBN;
+        const int32_t cnt = min(kBN, total - v0);
+        // one contiguous segment: uniform base
+        int32_t base = -1;
+        if (v0 + cnt <= b1) base = s0 + v0;
+        else if (v0 >= b2 && v0 + cnt <= b3) base = sa + (v0 - b2);
+        else if (v0 >= b3) base = sb + (v0 - b3);
+        const uint32_t kl = klds0 + buf * G::STAGEB, vl = vlds0 + buf * G::STAGEB;
+        if (base >= 0 && cnt == kBN) {
+            // a full stage of contiguous keys: one uniform offset
+            const int32_t kb0 = base * krow_b, vb0 = base * vrow_b;
+#pragma unroll
+            for (int j = 0; j < G::IPW; ++j) {
+                dma16(krs, kl + j * 1024, kb0 + koff[j]);
+                dma16(vrs, vl + j * 1024, vb0 + voff[j]);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < G::IPW; ++j) {
+                // absent rows of a ragged stage re-read a present row (masked)
+                const int32_t rr = min(srow[j], cnt - 1);
+                const int32_t key = base >= 0 ? base + rr : list_seq(v0 + rr, b1, b2, b3, s0, sa, sb, sm.sp);
+                dma16(krs, kl + j * 1024, key * krow_b + kcol[j]);
+                dma16(vrs, vl + j * 1024, key * vrow_b + vcol[j]);
+            }
+        }
+        if (!stage_fast(i) && tid < kBN) {
+            const int32_t v = v0 + tid;
+            int32_t inf = kKeyInvalid;
+            if (v < total) {
+                inf = kKeyAll;
+                if (label_mask && v >= b2) {
+                    const int32_t seq = list_seq(v, b1, b2, b3, s0, sa, sb, sm.sp);
+                    if (!is_shared_seq(sm.sp, seq)) inf = tile_label(seq - a.n_txt, o, a.tile, a.n_img);
+                }
+            }
+            sm.info[buf][tid] = inf;
+        }
+    };
+
+    // Operand addresses within a stage buffer.
+    // K: row 32 kt + ql, chunk 2 kc + h stored at (2 kc + h) ^ fk(row); fk
+    //    does not depend on kt, so the address is ka ^ (32 kc) + kt 32 ROWB.
+    const int ka = ql * G::ROWB + ((h ^ G::fk(ql)) * 16);
+    // V (transposing reads): lane (group gi = lane/16, j = lane%16) reads row
+    //    16 cc + 8 rd + 4 h + j/4, elements 32 dt + 16 (gi%2) + 4 (j%4) .. +4,
+    //    i.e. chunk 4 dt + 2 (gi%2) + (j%4)/2, half (j%4)%2; fv(row) does not
+    //    depend on cc, rd: address = va ^ (64 dt) + (16 cc + 8 rd) ROWB.
+    const int gi = lane >> 4, jj = lane & 15;
+    const int vrow = 4 * h + (jj >> 2);
+    const int va = vrow * G::ROWB + (((2 * (gi & 1) + ((jj & 3) >> 1)) ^ G::fv(vrow)) * 16) + ((jj & 3) & 1) * 8;
+
     f32x16 acc[D / 32];
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt) acc[dt] = f32x16{};
-    float m_run = -INFINITY;  // reference max of the scaled logits, log2 units
-    float l_run = 0.f;        // this lane's share of the running sum
+    float m_run = -INFINITY;         // reference max of the scaled logits, log2 units
+    float lp[4] = {0.f, 0.f, 0.f, 0.f};  // this lane's share of the running sum, by key chunk
     const float c = a.scale_log2;
 
-    // Stage i is consumed from LDS buffer i&1.  At the top of iteration i the
-    // registers hold stage i+1; they go to the other buffer and stage i+2 is
-    // requested, so its loads are in flight while stage i is computed.
-    Loader2<D> ld;
-    ld.init(kbase, vbase, a);
-    const int nblk = g.e3;
-    ld.load(BLOCK_AT(kBN2, 0, g, mc.label_mask), mc, a, sm.sp, tid, n_shared);
-    ld.store(sm.st, 0, tid);
-    if (nblk > 1) ld.load(BLOCK_AT(kBN2, 1, g, mc.label_mask), mc, a, sm.sp, tid, n_shared);
+    // Q has landed before any stage is requested: afterwards the only
+    // outstanding vector-memory operations are stage loads
+    wait_vmcnt<0>();
+    load_stage(0, 0);
+    wait_vmcnt<0>();
     __syncthreads();
-    for (int i = 0; i < nblk; ++i) {
+
+    for (int32_t i = 0; i < nblk; ++i) {
         const int buf = i & 1;
-        if (i + 1 < nblk) ld.store(sm.st, buf ^ 1, tid);
-        if (i + 2 < nblk) ld.load(BLOCK_AT(kBN2, i + 2, g, mc.label_mask), mc, a, sm.sp, tid, n_shared);
-        const Block b = BLOCK_AT(kBN2, i, g, mc.label_mask);
-        // S^T: s[kt] register e holds key 32 kt + 8 (e/4) + 4 h + e%4
-        f32x16 s[2];
+        if (i + 1 < nblk) load_stage(i + 1, buf ^ 1);
+        const uint8_t* kb_ = sm.k[buf];
+        const uint8_t* vb_ = sm.v[buf];
+
+        // S^T: s[kt] register e holds key 32 kt + 8 (e/4) + 4 h + e%4.  All
+        // K operands are requested first, so the MFMAs only wait for the
+        // first ones to arrive.
+        bf16x8 kop[D / 16][2];
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-            f32x16 t = {};
+        for (int kc = 0; kc < D / 16; ++kc)
 #pragma unroll
-            for (int kc = 0; kc < D / 16; ++kc) {
-                const bf16x8 k = *reinterpret_cast<const bf16x8*>(&sm.st.k[buf][32 * kt + ql][16 * kc + 8 * h]);
-                t = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k, q[kc], t, 0, 0, 0);
+            for (int kt = 0; kt < 2; ++kt)
+                kop[kc][kt] = *reinterpret_cast<const bf16x8*>(kb_ + (ka ^ (32 * kc)) + kt * 32 * G::ROWB);
+        __builtin_amdgcn_sched_barrier(0);
+        f32x16 s[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+        for (int kc = 0; kc < D / 16; ++kc)
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt)
+                s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kc][kt], q[kc], s[kt], 0, 0, 0);
+        // V^T operands of the whole stage, in flight during the softmax
+        bf16x8 vop[4][D / 32];
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+            for (int dt = 0; dt < D / 32; ++dt) {
+                const uint8_t* vp = vb_ + (va ^ (64 * dt)) + 16 * cc * G::ROWB;
+                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vp));
+                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vp + 8 * G::ROWB));
+                vop[cc][dt] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
             }
-            s[kt] = t;
-        }
-        if (!b.fast) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (!stage_fast(i)) {
 #pragma unroll
             for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
                 for (int e = 0; e < 16; ++e) {
-                    const int32_t inf = sm.st.info[buf][32 * kt + 8 * (e >> 2) + 4 * h + (e & 3)];
+                    const int32_t inf = sm.info[buf][32 * kt + 8 * (e >> 2) + 4 * h + (e & 3)];
                     s[kt][e] = (inf == kKeyAll || inf == ri.label) ? s[kt][e] : -INFINITY;
                 }
         }
-        float mx = -INFINITY;
+        // row max over the 64 keys: a tree of three-way maxima
+        float t3[11];
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt][e]);
-        mx = half_max(mx) * c;
+        for (int g = 0; g < 5; ++g) {
+            t3[g] = fmaxf(fmaxf(s[0][3 * g], s[0][3 * g + 1]), s[0][3 * g + 2]);
+            t3[5 + g] = fmaxf(fmaxf(s[1][3 * g], s[1][3 * g + 1]), s[1][3 * g + 2]);
+        }
+        t3[10] = fmaxf(s[0][15], s[1][15]);
+        const float u0 = fmaxf(fmaxf(t3[0], t3[1]), t3[2]);
+        const float u1 = fmaxf(fmaxf(t3[3], t3[4]), t3[5]);
+        const float u2 = fmaxf(fmaxf(t3[6], t3[7]), t3[8]);
+        const float u3 = fmaxf(t3[9], t3[10]);
+        const float mx = half_max(fmaxf(fmaxf(u0, u1), fmaxf(u2, u3))) * c;
         if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f)) {
             const float m_new = fmaxf(m_run, mx);
             // a row with every key masked so far keeps -inf: leave it alone
             const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
             m_run = m_new;
-            l_run *= alpha;
+#pragma unroll
+            for (int x = 0; x < 4; ++x) lp[x] *= alpha;
 #pragma unroll
             for (int dt = 0; dt < D / 32; ++dt) acc[dt] *= alpha;
         }
         const float m_use = m_run == -INFINITY ? 0.f : m_run;
-        // P = exp2(S c - m), rounded to bf16 for the PV product; chunk cc of
-        // 16 keys holds key 16 cc + 8 (j/4) + 4 h + j%4 in register j, i.e.
-        // V^T slot 16 cc + 8 h + j
+        // P = exp2(S c - m) rounded to bf16; chunk cc of 16 keys holds key
+        // 16 cc + 8 (j/4) + 4 h + j%4 in register j
         bf16x8 p[4];
 #pragma unroll
         for (int cc = 0; cc < 4; ++cc)
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const float pe = __builtin_amdgcn_exp2f(fmaf(s[cc >> 1][8 * (cc & 1) + j], c, -m_use));
-                l_run += pe;
+                lp[cc] += pe;
                 p[cc][j] = (__bf16)pe;
             }
 #pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt)
+        for (int cc = 0; cc < 4; ++cc)
 #pragma unroll
-            for (int cc = 0; cc < 4; ++cc) {
-                const bf16x8 v = *reinterpret_cast<const bf16x8*>(&sm.st.vt[buf][32 * dt + ql][16 * cc + 8 * h]);
-                acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v, p[cc], acc[dt], 0, 0, 0);
-            }
+            for (int dt = 0; dt < D / 32; ++dt)
+                acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[cc][dt], p[cc], acc[dt], 0, 0, 0);
+        // stage i+1 must have landed before anyone reads it, and every
+        // wavefront must be done with this buffer before it is refilled
+        wait_vmcnt<0>();
         __syncthreads();
     }
 
     __bf16* obase = reinterpret_cast<__bf16*>(a.o) + bb * a.o_sb + hh * a.o_sh;
+    const float l_run = (lp[0] + lp[1]) + (lp[2] + lp[3]);
     store_row<__bf16, D>(a, ri, bh, chunk, dense, h, m_run, l_run, acc, obase);
 }
 

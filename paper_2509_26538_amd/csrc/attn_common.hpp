@@ -14,8 +14,9 @@
 //                   continues at its head (the modular indexing of §3.2):
 //                   two contiguous segments, addressed in place.
 // Each key is visited once: shared keys that also lie in the rows' tiles are
-// masked in the shared segment.  Rows of shared tokens inside a sparse item
-// are computed by the dense items and not stored by the sparse item.
+// masked in the shared segment (fp32 kernel) or left out of it (bf16
+// kernel).  Rows of shared tokens inside a sparse item are computed by the
+// dense items and not stored by the sparse item.
 #pragma once
 
 #include "internal.hpp"
