@@ -57,7 +57,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--calls", type=int, default=20, help="per-call timings of each kernel")
+    ap.add_argument("--calls", type=int, default=50, help="per-call timings of each kernel")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -165,51 +165,109 @@ def main():
     achieved = sum(attn_flops) / (sum(attn_ms) * 1e-3) / 1e12
 
     # ------------------------------------------------------- per-call rows
-    def shape_report(wname, st_=None):
+    def spread(xs):
+        xs = sorted(xs)
+        at = lambda q: xs[min(len(xs) - 1, int(round(q * (len(xs) - 1))))]  # noqa: E731
+        return [round(at(0.1), 4), round(at(0.9), 4)]
+
+    def shape_report(wname, st_=None, calls=None, dense_calls=None):
         ww = synth.WORKLOADS[wname]
         s = st_ or setup(ww)
+        calls = calls or args.calls
+        dense_calls = dense_calls or calls
         hb.hilberta_schedule(s["cfg"], 1, s["sched"])
         nnz1 = nnz_from_table(ww, s["sched"].cpu().numpy())
         hb.hilberta_schedule(s["cfg"], 0, s["sched"])
         nnz0 = nnz_from_table(ww, s["sched"].cpu().numpy())
-        sp = per_call(lambda: hb.hilberta_attn_fwd(s["cfg"], s["sched"], s["q"], s["k"], s["v"], s["o"],
-                                                   workspace=s["ws"]), args.calls)
-        de = per_call(lambda: hb.dense_attn_fwd(s["q"], s["k"], s["v"], s["o"], workspace=s["dws"]),
-                      args.calls)
+        sparse = lambda: hb.hilberta_attn_fwd(s["cfg"], s["sched"], s["q"], s["k"], s["v"], s["o"],  # noqa: E731
+                                              workspace=s["ws"])
+        sparse()  # warm-up
+        sp = per_call(sparse, calls)
+        dense = lambda: hb.dense_attn_fwd(s["q"], s["k"], s["v"], s["o"], workspace=s["dws"])  # noqa: E731
+        dense()
+        de = per_call(dense, dense_calls)
         sp_ms, de_ms = statistics.median(sp), statistics.median(de)
         fl = 4 * ww.head_dim * ww.batch * ww.heads * nnz0
         fl_dense = 4 * ww.head_dim * ww.batch * ww.heads * ww.n_tot ** 2
-        return {
+        rep = {
             "shape": "%dx%d latent + %d text, %d heads, D %d" % (ww.grid, ww.grid, ww.n_txt, ww.heads,
                                                                ww.head_dim),
             "sparse_ms_per_call": round(sp_ms, 4),
+            "sparse_ms_p10_p90": spread(sp),
             "sparse_visited_tflops": round(fl / (sp_ms * 1e-3) / 1e12, 1),
+            "sparse_frac_bf16_peak": round(fl / (sp_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
             "sparse_gflop_per_call": round(fl / 1e9, 2),
             "nnz_per_head_layer0_layer1": [nnz0, nnz1],
             "dense_ms_per_call": round(de_ms, 4),
+            "dense_ms_p10_p90": spread(de),
             "dense_tflops": round(fl_dense / (de_ms * 1e-3) / 1e12, 1),
             "speedup_vs_dense": round(de_ms / sp_ms, 2),
+            "calls": [calls, dense_calls],
         }
+        return rep, s
 
-    rep128 = shape_report("flux-128", st)
+    rep128, _ = shape_report("flux-128", st)
     del st
     torch.cuda.empty_cache()
-    rep64 = shape_report("flux-64")
+    rep64, s64 = shape_report("flux-64")
+
+    # 57-layer sweep at 64x64: every block's slide offset, per-layer times
+    # against 57 dense calls
+    sw = synth.WORKLOADS["flux-64-sweep"]
+    per_layer = []
+    sweep_flops = 0
+    for layer in sw.layers:
+        hb.hilberta_schedule(s64["cfg"], layer, s64["sched"])
+        sweep_flops += 4 * sw.head_dim * sw.batch * sw.heads * nnz_from_table(sw, s64["sched"].cpu().numpy())
+        per_layer.append(statistics.median(per_call(
+            lambda: hb.hilberta_attn_fwd(s64["cfg"], s64["sched"], s64["q"], s64["k"], s64["v"], s64["o"],
+                                         workspace=s64["ws"]), 5)))
+    sweep = {
+        "layers": len(per_layer),
+        "per_layer_ms": [round(t, 4) for t in per_layer],
+        "total_ms": round(sum(per_layer), 3),
+        "dense_total_ms": round(len(per_layer) * rep64["dense_ms_per_call"], 3),
+        "speedup_vs_dense": round(len(per_layer) * rep64["dense_ms_per_call"] / sum(per_layer), 2),
+        "visited_tflops": round(sweep_flops / (sum(per_layer) * 1e-3) / 1e12, 1),
+    }
+    del s64
+    torch.cuda.empty_cache()
+    rep256, s256 = shape_report("stress-256", calls=10, dense_calls=3)
+    del s256
+    torch.cuda.empty_cache()
 
     # ------------------------------------------------------- token gather
+    # cold: a 512 MB write evicts the 256 MB last-level cache before each call
     flush = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device=dev)
-    gather_ms = []
-    for _ in range(args.calls):
-        flush.fill_(1)  # evict the 256 MB last-level cache
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        hb.hilberta_permute(x, y, perm)
-        b.record()
-        torch.cuda.synchronize()
-        gather_ms.append(a.elapsed_time(b))
-    del flush
-    gather_bytes = 2 * x.numel() * x.element_size() + perm.numel() * 4
-    gather_gbs = gather_bytes / (statistics.median(gather_ms) * 1e-3) / 1e9
+
+    def cold(fn, n):
+        ts = []
+        for _ in range(n):
+            flush.fill_(1)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        return statistics.median(ts)
+
+    def copy_report(xx, yy, pp):
+        nbytes = 2 * xx.numel() * xx.element_size() + pp.numel() * 4
+        g = cold(lambda: hb.hilberta_permute(xx, yy, pp), args.calls)
+        u = cold(lambda: hb.hilberta_unpermute(yy, xx, pp), args.calls)
+        return {"bytes": nbytes, "gather_ms_cold": round(g, 4), "scatter_ms_cold": round(u, 4),
+                "gather_GB/s": round(nbytes / (g * 1e-3) / 1e9, 1),
+                "scatter_GB/s": round(nbytes / (u * 1e-3) / 1e9, 1),
+                "gather_frac_hbm": round(nbytes / (g * 1e-3) / 1e9 / PEAK_HBM_GBS, 3)}
+
+    gather = {"128x128 [16384, 3072] bf16": copy_report(x, y, perm)}
+    x256 = synth.hidden_states(1, 256 * 256, w.hidden, "bf16", seed=2).to(dev)
+    y256 = torch.empty_like(x256)
+    perm256 = torch.empty(256 * 256, dtype=torch.int32, device=dev)
+    hb.hilberta_build_perm(256, 256, perm256)
+    gather["256x256 [65536, 3072] bf16"] = copy_report(x256, y256, perm256)
+    del flush, x256, y256
 
     # ------------------------------------------------------- HBM traffic
     traffic = None
@@ -260,8 +318,9 @@ def main():
         "cpu_baseline": cpu,
         "attn_128": rep128,
         "attn_64": rep64,
-        "gather": {"bytes": gather_bytes, "ms_cold": round(statistics.median(gather_ms), 4),
-                   "GB/s": round(gather_gbs, 1), "frac_hbm": round(gather_gbs / PEAK_HBM_GBS, 3)},
+        "sweep_64_57_layers": sweep,
+        "attn_256": rep256,
+        "gather": gather,
         "wall_s_timed": round(wall, 3),
     }
     print(json.dumps(out), flush=True)
@@ -296,7 +355,18 @@ def cpu_baseline(w):
                   "layer 1; %.1f s wall, %.2f GFLOP visited" % (len(rows), w.n_tot // n_rows, w.n_tot,
                                                                 w.heads, wall, flops / 1e9),
         "host_cpus": os.cpu_count(),
+        "cpu_model": cpu_model(),
     }
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 if __name__ == "__main__":

@@ -20,6 +20,9 @@ def as_bits(t):
 @pytest.mark.parametrize("side,batch,channels,dtype", [
     (16, 1, 64, "f32"), (16, 3, 64, "bf16"), (32, 2, 3072, "bf16"), (8, 2, 3, "bf16"),
     (8, 1, 5, "f32"), (64, 1, 3072, "bf16"), (2, 4, 8, "f32"),
+    # rows of at least 64 vectors take the one-row-per-wavefront kernel: a
+    # ragged last pass (125 and 150 16-byte vectors), 2- and 4-byte vectors
+    (16, 2, 1000, "bf16"), (16, 1, 600, "f32"), (8, 3, 1001, "bf16"), (4, 2, 4097, "f32"),
 ])
 def test_permute_unpermute_match_oracle(gpu, side, batch, channels, dtype):
     n = side * side
@@ -39,9 +42,10 @@ def test_permute_unpermute_match_oracle(gpu, side, batch, channels, dtype):
     assert np.array_equal(tokens.unpermute(ref_y, ref_perm), as_bits(x))
 
 
-def test_permute_image_rows_behind_text(gpu):
+@pytest.mark.parametrize("c", [128, 3072])
+def test_permute_image_rows_behind_text(gpu, c):
     # text rows stay in place: the call covers the image rows of [B, n_txt + N, C]
-    side, n_txt, c = 16, 7, 128
+    side, n_txt = 16, 7
     n = side * side
     x = synth.hidden_states(2, n_txt + n, c, "bf16", seed=3).to(gpu)
     perm = torch.empty(n, dtype=torch.int32, device=gpu)
