@@ -40,9 +40,9 @@ PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 N_LAYERS = 57              # Flux.1-dev: 19 double-stream + 38 single-stream blocks
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hilberta_attn_fwd_flux128_traffic.json")
-# sources the bf16 attention kernel is compiled from; counters taken on an
-# older build of them are not reported
-ATTN_SOURCES = ("attn_bf16.hip", "attn_common.hpp", "internal.hpp")
+# sources that decide the attention launch's kernels and work plan; counters
+# taken on an older build of them are not reported
+ATTN_SOURCES = ("attn_bf16.hip", "attn_common.hpp", "internal.hpp", "attn.hip", "abi.cpp")
 
 
 def attn_source_digest():

@@ -117,9 +117,11 @@ struct Plan {
         total_items, ws_bytes;
 };
 
-// Split long dense rows into key chunks about as long as a sparse item's key
-// list, so that no workgroup runs far longer than the rest; for the dense
-// baseline, split only when the rows alone would not fill the GPU a few times.
+// Split long dense rows into key chunks about twice as long as a sparse
+// item's key list: no workgroup runs far longer than the rest (dense items
+// come first in their head's item range), and the partials stay few.  For
+// the dense baseline, split only when the rows alone would not fill the GPU
+// a few times.
 Plan make_plan(bool sparse, int64_t n_txt, int64_t n_img, int64_t n_shared, int64_t tile,
                int64_t n_tot, int64_t bh, int64_t head_dim, int dtype, bool allow_split) {
     Plan p{};
@@ -131,7 +133,7 @@ Plan make_plan(bool sparse, int64_t n_txt, int64_t n_img, int64_t n_shared, int6
         p.sparse_blocks = ceil_div(n_img, bm);
         const int64_t sparse_keys = round_up(n_txt, bn) + round_up(n_shared, bn) +
                                     round_up(tile < n_img ? tile : n_img, bn);
-        chunk = round_up(sparse_keys > 512 ? sparse_keys : 512, bn);
+        chunk = round_up(2 * (sparse_keys > 512 ? sparse_keys : 512), bn);
     } else {
         p.n_dense_rows = n_tot;
         p.sparse_blocks = 0;

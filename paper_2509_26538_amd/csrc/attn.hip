@@ -206,14 +206,20 @@ __global__ void __launch_bounds__(kThreads, 1) attn_f32_kernel(AttnArgs a) {
 // (acc_c, m_c, l_c), M = max m_c, L = sum l_c 2^(m_c - M) and
 // O = sum acc_c 2^(m_c - M) / L -- the same rescaling Algorithm 1 applies
 // between key blocks.  One wavefront per row.
+// Split-K merge of the dense rows.  A row is handled by 32 lanes, each owning
+// four consecutive elements (16-byte loads); a wavefront merges two rows.
+// The chunks' (m, l) are read by one lane per chunk and combined with
+// cross-lane reductions; the partial accumulators are streamed with
+// non-temporal loads, four chunks in flight.
 template <typename T, int D>
 __global__ void __launch_bounds__(256) merge_kernel(MergeArgs m) {
-    constexpr int EPL = D / 64;  // elements per lane
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int64_t rowid = (int64_t)blockIdx.x * 4 + wave;
-    if (rowid >= (int64_t)m.n_bh * m.n_dense_rows) return;
-    const int32_t bh = (int32_t)(rowid / m.n_dense_rows);
-    const int32_t r = (int32_t)(rowid - (int64_t)bh * m.n_dense_rows);
+    constexpr int LPR = D / 4;  // lanes per row
+    constexpr int RPB = 256 / LPR;
+    const int sub = threadIdx.x % LPR;
+    const int64_t rowid = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
+    const bool valid_row = rowid < (int64_t)m.n_bh * m.n_dense_rows;
+    const int32_t bh = valid_row ? (int32_t)(rowid / m.n_dense_rows) : 0;
+    const int32_t r = valid_row ? (int32_t)(rowid - (int64_t)bh * m.n_dense_rows) : 0;
     int32_t seq = r;
     if (m.sparse && r >= m.n_txt) {
         const int32_t n_sp = min(max(m.sched[6], 0), min(m.span_cap, kMaxSpans));
@@ -229,33 +235,55 @@ __global__ void __launch_bounds__(256) merge_kernel(MergeArgs m) {
             }
             u -= ln;
         }
-        if (seq < 0) return;
     }
+    const bool active = valid_row && seq >= 0;
     const float* ml = m.ws + (int64_t)m.n_bh * m.n_chunks * m.n_dense_rows * D;
     const int64_t slot0 = (int64_t)bh * m.n_chunks * m.n_dense_rows + r;
+    // global max of the chunks' m, then L = sum_c 2^(m_c - M) l_c
     float mx = -INFINITY;
-    for (int c = 0; c < m.n_chunks; ++c) mx = fmaxf(mx, ml[(slot0 + (int64_t)c * m.n_dense_rows) * 2]);
+    for (int32_t c = sub; c < m.n_chunks; c += LPR)
+        if (active) mx = fmaxf(mx, ml[(slot0 + (int64_t)c * m.n_dense_rows) * 2]);
+#pragma unroll
+    for (int off = LPR / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, LPR));
     const float m_use = mx == -INFINITY ? 0.f : mx;
     float L = 0.f;
-    float o[EPL];
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) o[e] = 0.f;
-    for (int c = 0; c < m.n_chunks; ++c) {
+    for (int32_t c = sub; c < m.n_chunks; c += LPR) {
+        if (!active) break;
         const int64_t slot = slot0 + (int64_t)c * m.n_dense_rows;
-        const float w = __builtin_amdgcn_exp2f(ml[slot * 2] - m_use);
-        L += w * ml[slot * 2 + 1];
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) o[e] += w * m.ws[slot * D + lane * EPL + e];
+        L += __builtin_amdgcn_exp2f(ml[slot * 2] - m_use) * ml[slot * 2 + 1];
     }
+#pragma unroll
+    for (int off = LPR / 2; off > 0; off >>= 1) L += __shfl_xor(L, off, LPR);
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    f4 o = {0.f, 0.f, 0.f, 0.f};
+    if (active) {
+        int32_t c = 0;
+        for (; c + 4 <= m.n_chunks; c += 4) {
+            f4 part[4];
+            float w[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int64_t slot = slot0 + (int64_t)(c + k) * m.n_dense_rows;
+                part[k] = __builtin_nontemporal_load(reinterpret_cast<const f4*>(m.ws + slot * D) + sub);
+                w[k] = __builtin_amdgcn_exp2f(ml[slot * 2] - m_use);
+            }
+#pragma unroll
+            for (int k = 0; k < 4; ++k) o += w[k] * part[k];
+        }
+        for (; c < m.n_chunks; ++c) {
+            const int64_t slot = slot0 + (int64_t)c * m.n_dense_rows;
+            const f4 part = __builtin_nontemporal_load(reinterpret_cast<const f4*>(m.ws + slot * D) + sub);
+            o += __builtin_amdgcn_exp2f(ml[slot * 2] - m_use) * part;
+        }
+    }
+    if (!active) return;
     const float inv = L > 0.f ? 1.f / L : 0.f;
     const int32_t b = bh / m.heads, hh = bh - b * m.heads;
     T* orow = reinterpret_cast<T*>(m.o) + b * m.o_sb + hh * m.o_sh + (int64_t)seq * m.o_sr;
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) orow[lane * EPL + e] = (T)(o[e] * inv);
-    if (m.lse && lane == 0)
+    store4<T>(orow + 4 * sub, o[0] * inv, o[1] * inv, o[2] * inv, o[3] * inv);
+    if (m.lse && sub == 0)
         m.lse[(int64_t)bh * m.n_tot + seq] = L > 0.f ? (m_use + log2f(L)) * kLn2 : -INFINITY;
 }
-
 template <int D>
 hipError_t launch_f32(const AttnArgs& a, hipStream_t s) {
     hipLaunchKernelGGL((attn_f32_kernel<D>), dim3(a.total_items), dim3(kThreads), 0, s, a);
@@ -265,7 +293,8 @@ hipError_t launch_f32(const AttnArgs& a, hipStream_t s) {
 template <typename T, int D>
 hipError_t launch_merge_t(const MergeArgs& m, hipStream_t s) {
     const int64_t rows = (int64_t)m.n_bh * m.n_dense_rows;
-    const int64_t blocks = (rows + 3) / 4;
+    constexpr int64_t rpb = 256 / (D / 4);
+    const int64_t blocks = (rows + rpb - 1) / rpb;
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
     hipLaunchKernelGGL((merge_kernel<T, D>), dim3((unsigned)blocks), dim3(256), 0, s, m);
