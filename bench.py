@@ -232,6 +232,43 @@ def main():
     }
     del s64
     torch.cuda.empty_cache()
+
+    # the paper's Table 1 settings (4 or 16 tiles, slide cycle 4, 16x16 or
+    # 32x32 shared region), against the dense baseline of the same shape
+    table1 = {}
+    dense_ms = {64: rep64["dense_ms_per_call"], 128: rep128["dense_ms_per_call"]}
+    for name in ("table1-64-g4", "table1-64-g16", "table1-128-g4", "table1-128-g16"):
+        tw = synth.WORKLOADS[name]
+        ts = setup(tw)
+        ms, fl = [], []
+        for layer in (0, 1):
+            hb.hilberta_schedule(ts["cfg"], layer, ts["sched"])
+            fl.append(4 * tw.head_dim * tw.batch * tw.heads * nnz_from_table(tw, ts["sched"].cpu().numpy()))
+            call = lambda: hb.hilberta_attn_fwd(ts["cfg"], ts["sched"], ts["q"], ts["k"], ts["v"], ts["o"],  # noqa: E731
+                                                workspace=ts["ws"])
+            call()
+            ms.append(statistics.median(per_call(call, 20)))
+        t_ms = statistics.fmean(ms)
+        g = tw.n_img // tw.tile
+        n_sh = tw.shared * tw.shared
+        # the paper's FLOP accounting for this table: prefix keys for the
+        # non-shared image rows plus the tiles, no dense rows
+        paper_gflop = 4 * tw.heads * tw.head_dim * ((tw.n_img - n_sh) * (tw.n_txt + n_sh) + tw.n_img ** 2 // g) / 1e9
+        table1[name] = {
+            "tiles": g, "tile": tw.tile, "delta": tw.delta, "shared": "%dx%d" % (tw.shared, tw.shared),
+            "sparse_ms_per_call": round(t_ms, 4),
+            "visited_tflops": round(statistics.fmean(fl) / (t_ms * 1e-3) / 1e12, 1),
+            "speedup_vs_dense": round(dense_ms[tw.grid] / t_ms, 2),
+            "paper_accounting_gflop": round(paper_gflop, 1),
+        }
+        del ts
+        torch.cuda.empty_cache()
+    # the paper's own A100 measurements of these rows (another machine; context only)
+    table1["paper_a100_context"] = {
+        "1024^2": {"dense_ms": 1.42, "4_tiles_ms": 0.78, "16_tiles_ms": 0.62, "speedups": [1.82, 2.30]},
+        "2048^2": {"dense_ms": 18.14, "4_tiles_ms": 7.37, "16_tiles_ms": 4.36, "speedups": [2.47, 4.17]},
+    }
+
     rep256, s256 = shape_report("stress-256", calls=10, dense_calls=3)
     del s256
     torch.cuda.empty_cache()
@@ -319,6 +356,7 @@ def main():
         "attn_128": rep128,
         "attn_64": rep64,
         "sweep_64_57_layers": sweep,
+        "paper_table1_settings": table1,
         "attn_256": rep256,
         "gather": gather,
         "wall_s_timed": round(wall, 3),

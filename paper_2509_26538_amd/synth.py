@@ -54,6 +54,13 @@ WORKLOADS = {
     "flux-128": Workload("flux-128", 128, 512, 1, 24, 128, "bf16", 1024, 512, 16),
     # 4096x4096 stress shape: 256x256 latent grid plus 512 text tokens
     "stress-256": Workload("stress-256", 256, 512, 1, 24, 128, "bf16", 2048, 1024, 32),
+    # the settings of the paper's Table 1: G = 4 or 16 tiles (N_T = N_img/G),
+    # a slide cycle of 4 (Delta = N_T/4), a 16x16 shared region at 1024x1024
+    # and 32x32 at 2048x2048
+    "table1-64-g4": Workload("table1-64-g4", 64, 512, 1, 24, 128, "bf16", 1024, 256, 16),
+    "table1-64-g16": Workload("table1-64-g16", 64, 512, 1, 24, 128, "bf16", 256, 64, 16),
+    "table1-128-g4": Workload("table1-128-g4", 128, 512, 1, 24, 128, "bf16", 4096, 1024, 32),
+    "table1-128-g16": Workload("table1-128-g16", 128, 512, 1, 24, 128, "bf16", 1024, 256, 32),
 }
 
 

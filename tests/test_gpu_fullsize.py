@@ -134,3 +134,17 @@ def test_stress256_sampled_rows(gpu):
         r.check_rows(o, layer, sample_rows(r.layout, layer, n_random=8), "layer %d" % layer)
     del r
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", ["table1-64-g4", "table1-64-g16", "table1-128-g4", "table1-128-g16"])
+def test_paper_table1_settings(gpu, name):
+    # the paper's own settings (4 or 16 tiles, slide cycle 4, 16x16 or 32x32
+    # shared region): with Delta = N_T/4 a 128-row block can straddle two
+    # tiles, which takes the per-row tile masks
+    r = Resident(name, gpu)
+    for layer in (0, 1, 2, 3):
+        o = r.run(layer)
+        r.check_all(o, "%s layer %d" % (name, layer))
+        r.check_rows(o, layer, sample_rows(r.layout, layer, n_random=8, seed=7), "%s layer %d" % (name, layer))
+    del r
+    torch.cuda.empty_cache()
