@@ -76,14 +76,16 @@ def main():
     torch.cuda.set_device(dev)
 
     def tables(w):
-        cfg = hb.make_config(w.grid, w.n_txt, w.tile, w.delta, w.shared)
+        cfg = hb.make_config(w.grid, w.n_txt, w.tile, w.delta, w.shared,
+                             layout=hb.LAYOUT_MOVED if w.moved else hb.LAYOUT_IN_PLACE)
         words = hb.hilberta_schedule_words(cfg)
         return cfg, words
 
     def nnz_from_table(w, tab):
         # tab: host copy of the schedule table; tile entries carry the shared
-        # tokens inside each tile
-        n_glob = w.n_txt + w.shared * w.shared
+        # tokens inside each tile (none when the shared tokens are moved into
+        # the global prefix)
+        n_glob = int(tab[1]) + (0 if w.moved else w.shared * w.shared)
         total = n_glob * w.n_tot
         T = int(tab[4])
         for q in range(T):
@@ -234,10 +236,12 @@ def main():
     torch.cuda.empty_cache()
 
     # the paper's Table 1 settings (4 or 16 tiles, slide cycle 4, 16x16 or
-    # 32x32 shared region), against the dense baseline of the same shape
+    # 32x32 shared region), in place and with the shared tokens moved into the
+    # global prefix, against the dense baseline of the same shape
     table1 = {}
     dense_ms = {64: rep64["dense_ms_per_call"], 128: rep128["dense_ms_per_call"]}
-    for name in ("table1-64-g4", "table1-64-g16", "table1-128-g4", "table1-128-g16"):
+    for name in ("table1-64-g4", "table1-64-g16", "table1-128-g4", "table1-128-g16",
+                 "moved-64-g4", "moved-64-g16", "moved-128-g4", "moved-128-g16"):
         tw = synth.WORKLOADS[name]
         ts = setup(tw)
         ms, fl = [], []
@@ -249,12 +253,13 @@ def main():
             call()
             ms.append(statistics.median(per_call(call, 20)))
         t_ms = statistics.fmean(ms)
-        g = tw.n_img // tw.tile
         n_sh = tw.shared * tw.shared
+        g = (tw.n_img - (n_sh if tw.moved else 0)) // tw.tile
         # the paper's FLOP accounting for this table: prefix keys for the
         # non-shared image rows plus the tiles, no dense rows
-        paper_gflop = 4 * tw.heads * tw.head_dim * ((tw.n_img - n_sh) * (tw.n_txt + n_sh) + tw.n_img ** 2 // g) / 1e9
+        paper_gflop = 4 * tw.heads * tw.head_dim * ((tw.n_img - n_sh) * (tw.n_txt + n_sh) + g * tw.tile ** 2) / 1e9
         table1[name] = {
+            "layout": "moved" if tw.moved else "in_place",
             "tiles": g, "tile": tw.tile, "delta": tw.delta, "shared": "%dx%d" % (tw.shared, tw.shared),
             "sparse_ms_per_call": round(t_ms, 4),
             "visited_tflops": round(statistics.fmean(fl) / (t_ms * 1e-3) / 1e12, 1),

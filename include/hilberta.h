@@ -51,6 +51,10 @@ extern "C" {
 /* first word of every schedule table */
 #define HILBERTA_SCHEDULE_MAGIC 0x48424131
 
+/* Sequence layouts (hilberta_config.layout). */
+#define HILBERTA_LAYOUT_IN_PLACE 0 /* shared tokens keep their Hilbert slots */
+#define HILBERTA_LAYOUT_MOVED 1    /* shared tokens gathered next to the text */
+
 /*
  * Geometry of one HilbertA attention layer stack.
  *   grid_h, grid_w   latent grid; must be square with a power-of-two side in
@@ -63,6 +67,15 @@ extern "C" {
  *                    [(side - s)/2, (side - s)/2 + s), integer halving; 0 x 0
  *                    disables it.  At most 1024 shared tokens (32 x 32,
  *                    the largest region the paper uses).
+ *   layout           HILBERTA_LAYOUT_IN_PLACE: the image span keeps all N_img
+ *                    tokens in Hilbert order, the shared ones in their slots
+ *                    (also global keys and dense rows), and is tiled whole.
+ *                    HILBERTA_LAYOUT_MOVED (Appendix A taken literally): the
+ *                    image span holds the N_sh shared tokens first, then the
+ *                    others, each part in Hilbert order (see
+ *                    hilberta_build_perm_layout); the global prefix is the
+ *                    text and the shared tokens, and only the N_img - N_sh
+ *                    others are tiled, so `tile` must divide N_img - N_sh.
  * The sequence must satisfy n_txt + grid_h*grid_w < 2^31.
  */
 typedef struct hilberta_config {
@@ -73,6 +86,7 @@ typedef struct hilberta_config {
     int32_t delta;
     int32_t shared_h;
     int32_t shared_w;
+    int32_t layout;
 } hilberta_config;
 
 /* Library version (major*10000 + minor*100 + patch). Host only. */
@@ -92,6 +106,18 @@ const char* hilberta_last_error(void);
  */
 int hilberta_build_perm(int32_t grid_h, int32_t grid_w, int32_t* perm,
                         int32_t* inv_or_null, void* stream);
+
+/*
+ * hilberta_build_perm_layout -- the image-span order of cfg's layout: the
+ *   Hilbert linearisation (as hilberta_build_perm) in place; moved, the
+ *   shared tokens first and then the others, each part in Hilbert order
+ *   (Appendix A gathers the shared tokens next to the text).  perm[d] is the
+ *   raster index of the token at image-span position d; if inv_or_null is
+ *   not NULL, inv[perm[d]] = d.  perm, inv: device int32[grid_h*grid_w].
+ * Errors: as hilberta_schedule_words for cfg; EINVAL (perm NULL).
+ */
+int hilberta_build_perm_layout(const hilberta_config* cfg, int32_t* perm,
+                               int32_t* inv_or_null, void* stream);
 
 /*
  * hilberta_permute -- the token gather of §3.4, applied once at the input:
@@ -126,18 +152,21 @@ int hilberta_schedule_words(const hilberta_config* cfg, int64_t* words);
 /*
  * hilberta_schedule -- the per-layer tile schedule of §3.2 and the shared
  * runs of §3.3, written to device memory `sched` (int32[capacity]).
- *   Layer l slides the boundaries by o = (l*delta) mod N_img: image position
- *   p has tile label floor((p + l*delta)/N_T) mod T, queries and keys of equal
- *   label attend each other, and the wrap-around tile is read with modular
- *   indexing (§3.2), never copied.
+ *   Layer l slides the boundaries by o = (l*delta) mod N: position p of the
+ *   tiled span has tile label floor((p + l*delta)/N_T) mod T, queries and
+ *   keys of equal label attend each other, and the wrap-around tile is read
+ *   with modular indexing (§3.2), never copied.  In place the global prefix
+ *   P is the text and the tiled span is the whole image (N = N_img); moved,
+ *   P = n_txt + N_sh and N = N_img - N_sh, and there are no shared runs.
  *   Table layout (int32 words):
- *     [0] HILBERTA_SCHEDULE_MAGIC  [1] n_txt  [2] N_img  [3] N_T  [4] T
+ *     [0] HILBERTA_SCHEDULE_MAGIC  [1] P  [2] N  [3] N_T  [4] T
  *     [5] o  [6] n_spans  [7] n_shared  [8] layer  [9] grid_h  [10] grid_w
- *     [11] span capacity C = shared_h + shared_w + 1 (0 without a region)
+ *     [11] span capacity C = shared_h + shared_w + 1 (0 without a region
+ *          or when moved)
  *     [12 + 4q .. 12 + 4q + 3], q < T: tile q as (start, len1, len2, ns):
  *         its tokens are [start, start + len1) and, when it wraps past the
- *         end of the sequence, [n_txt, n_txt + len2); start is a sequence
- *         position; ns = shared tokens inside the tile.
+ *         end of the sequence, [P, P + len2); start is a sequence position;
+ *         ns = shared tokens inside the tile (0 when moved).
  *     [12 + 4T + 2s, +1], s < C: shared run s as (start, len), sequence
  *         positions, ascending, maximal; zero past n_spans.
  *   The table has exactly hilberta_schedule_words(cfg) words.

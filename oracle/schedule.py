@@ -19,6 +19,12 @@ open (each reading is listed in the design notes):
   them and they attend every token, like the text tokens (Appendix A).
 * Mask (explicit, dense): M[i, j] = 1 iff i is a text/shared token, or j is
   a text/shared token, or i and j are image tokens with equal labels.
+
+The moved-prefix layout (``Layout.moved``) takes Appendix A literally
+instead: the shared tokens are gathered next to the text, so the global
+prefix is [0, n_txt + N_sh) (text, then the shared tokens in Hilbert order),
+and only the N_img - N_sh other image tokens, in Hilbert order, are tiled:
+the tile size N_T divides N_img - N_sh and the labels run over that span.
 """
 
 from dataclasses import dataclass
@@ -43,6 +49,7 @@ class Layout:
     delta: int         # per-layer advance Delta
     shared_h: int = 0  # central shared region, rows
     shared_w: int = 0  # central shared region, columns
+    moved: bool = False  # shared tokens gathered next to the text (Appendix A literally)
 
     @property
     def n_img(self):
@@ -53,20 +60,36 @@ class Layout:
         return self.n_txt + self.n_img
 
     @property
+    def n_shared(self):
+        return self.shared_h * self.shared_w
+
+    @property
+    def prefix(self):
+        """Global prefix: the text, plus the shared tokens when they are moved."""
+        return self.n_txt + (self.n_shared if self.moved else 0)
+
+    @property
+    def tiled(self):
+        """Tokens in the tiled span: all image tokens, or the non-shared ones."""
+        return self.n_img - (self.n_shared if self.moved else 0)
+
+    @property
     def n_tiles(self):
-        if self.n_img % self.tile:
-            raise ValueError("the tile size must divide the image token count")
-        return self.n_img // self.tile
+        if self.tiled % self.tile:
+            raise ValueError("the tile size must divide the tiled token count")
+        return self.tiled // self.tile
 
 
 def offset(layout, layer):
-    """o_l = (l * Delta) mod N_img: how far the tile boundaries have slid."""
-    return (layer * layout.delta) % layout.n_img
+    """o_l = (l * Delta) mod N: how far the tile boundaries have slid (N the
+    tiled token count)."""
+    return (layer * layout.delta) % layout.tiled
 
 
 def labels(layout, layer):
-    """q_p(l) for every image position p, by the literal formula of §3.2."""
-    p = np.arange(layout.n_img, dtype=np.int64)
+    """q_p(l) for every position p of the tiled span, by the literal formula
+    of §3.2."""
+    p = np.arange(layout.tiled, dtype=np.int64)
     return ((p + layer * layout.delta) // layout.tile) % layout.n_tiles
 
 
@@ -86,6 +109,16 @@ def shared_hilbert(layout):
     """Boolean over Hilbert positions p: True where token perm[p] is shared."""
     perm, _ = hilbert.build_perm(layout.grid_h, layout.grid_w)
     return shared_raster(layout)[perm]
+
+
+def moved_perm(layout):
+    """Image-span order of the moved-prefix layout: perm[d] is the raster
+    index of the token at image-span position d.  The shared tokens come
+    first, in Hilbert order, then the other image tokens, in Hilbert order.
+    """
+    hperm, _ = hilbert.build_perm(layout.grid_h, layout.grid_w)
+    sh = shared_raster(layout)[hperm]
+    return np.concatenate([hperm[sh], hperm[~sh]])
 
 
 def runs(flags):
@@ -109,7 +142,7 @@ def max_spans(layout):
     Each run but one is entered and left across a distinct edge of the
     region's boundary, which has 2 (shared_h + shared_w) edges.
     """
-    if layout.shared_h * layout.shared_w == 0:
+    if layout.shared_h * layout.shared_w == 0 or layout.moved:
         return 0
     return layout.shared_h + layout.shared_w + 1
 
@@ -119,16 +152,17 @@ def table_words(layout):
 
 
 def tiles(layout, layer):
-    """Per tile q: (start, len1, len2, n_shared) in image coordinates.
+    """Per tile q: (start, len1, len2, n_shared) in tiled-span coordinates.
 
     Found by scanning the labels, not from a closed form: the members of tile
     q form one cyclic run; ``start`` is the member whose predecessor (cyclic)
-    is not a member, len1 runs to the end of the image span and len2 > 0 only
-    when the run wraps to position 0.
+    is not a member, len1 runs to the end of the span and len2 > 0 only when
+    the run wraps to position 0.  n_shared counts the shared tokens inside
+    the tile (none in the moved-prefix layout).
     """
     lab = labels(layout, layer)
-    sh = shared_hilbert(layout)
-    n = layout.n_img
+    sh = np.zeros(layout.tiled, dtype=bool) if layout.moved else shared_hilbert(layout)
+    n = layout.tiled
     out = []
     for q in range(layout.n_tiles):
         members = np.nonzero(lab == q)[0]
@@ -153,25 +187,28 @@ def schedule_table(layout, layer):
     """The int32 schedule table of hilberta_schedule, built from the scans above.
 
     Layout (all int32):
-      [0] magic  [1] n_txt  [2] n_img  [3] N_T  [4] T  [5] o_l  [6] n_spans
-      [7] n_shared  [8] layer  [9] grid_h  [10] grid_w  [11] span capacity
+      [0] magic  [1] global prefix length  [2] tiled tokens  [3] N_T  [4] T
+      [5] o_l  [6] n_spans  [7] n_shared  [8] layer  [9] grid_h  [10] grid_w
+      [11] span capacity
       then T x (start, len1, len2, n_shared_in_tile), start in sequence
-      coordinates (n_txt + image position),
+      coordinates (prefix + span position),
       then capacity x (start, len) shared runs in sequence coordinates,
-      ascending, zero-filled past n_spans.
+      ascending, zero-filled past n_spans (none in the moved layout).
+    The prefix is n_txt and the tiled span all N_img image tokens in place;
+    moved, the prefix is n_txt + n_shared and the span the other tokens.
     """
     sh_runs = runs(shared_hilbert(layout)) if max_spans(layout) else []
     cap = max_spans(layout)
     assert len(sh_runs) <= cap
     t = np.zeros(table_words(layout), dtype=np.int64)
     t[0] = TABLE_MAGIC
-    t[1] = layout.n_txt
-    t[2] = layout.n_img
+    t[1] = layout.prefix
+    t[2] = layout.tiled
     t[3] = layout.tile
     t[4] = layout.n_tiles
     t[5] = offset(layout, layer)
     t[6] = len(sh_runs)
-    t[7] = sum(r[1] for r in sh_runs)
+    t[7] = layout.n_shared if layout.moved else sum(r[1] for r in sh_runs)
     t[8] = layer
     t[9] = layout.grid_h
     t[10] = layout.grid_w
@@ -179,7 +216,7 @@ def schedule_table(layout, layer):
     base = HEADER_WORDS
     for q, (start, len1, len2, nsh) in enumerate(tiles(layout, layer)):
         t[base + TILE_WORDS * q: base + TILE_WORDS * (q + 1)] = (
-            layout.n_txt + start, len1, len2, nsh)
+            layout.prefix + start, len1, len2, nsh)
     base += TILE_WORDS * layout.n_tiles
     for s, (start, ln) in enumerate(sh_runs):
         t[base + SPAN_WORDS * s: base + SPAN_WORDS * (s + 1)] = (layout.n_txt + start, ln)
@@ -191,14 +228,16 @@ def token_classes(layout, layer):
     """Per sequence position: (is_global, label).
 
     is_global marks text tokens and shared tokens (the global prefix of
-    Appendix A); label is the layer-l tile label of image tokens and -1 for
-    text tokens.
+    Appendix A); label is the layer-l tile label of the tokens of the tiled
+    span and -1 for the others.  In place, shared tokens are global and
+    labelled; moved, they are part of the prefix.
     """
     is_global = np.zeros(layout.n_tot, dtype=bool)
-    is_global[:layout.n_txt] = True
-    is_global[layout.n_txt:] = shared_hilbert(layout)
     lab = np.full(layout.n_tot, -1, dtype=np.int64)
-    lab[layout.n_txt:] = labels(layout, layer)
+    is_global[:layout.prefix] = True
+    if not layout.moved:
+        is_global[layout.n_txt:] = shared_hilbert(layout)
+    lab[layout.prefix:] = labels(layout, layer)
     return is_global, lab
 
 

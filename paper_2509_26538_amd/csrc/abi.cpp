@@ -38,6 +38,8 @@ int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 
 int check_config(const hilberta_config* c) {
     if (!c) return fail(HILBERTA_EINVAL, "config is NULL");
+    if (c->layout != HILBERTA_LAYOUT_IN_PLACE && c->layout != HILBERTA_LAYOUT_MOVED)
+        return fail(HILBERTA_EINVAL, "layout %d is neither in place (0) nor moved (1)", c->layout);
     if (c->grid_h != c->grid_w)
         return fail(HILBERTA_EUNSUPPORTED, "grid %dx%d is not square", c->grid_h, c->grid_w);
     if (!pow2(c->grid_w) || c->grid_w < 2 || c->grid_w > 32768)
@@ -48,7 +50,7 @@ int check_config(const hilberta_config* c) {
     if (c->n_txt + n_img > 0x7fffffffLL)
         return fail(HILBERTA_EUNSUPPORTED, "sequence of %lld tokens is too long",
                     (long long)(c->n_txt + n_img));
-    if (c->tile < 1 || n_img % c->tile)
+    if (c->tile < 1 || (c->layout != HILBERTA_LAYOUT_MOVED && n_img % c->tile))
         return fail(HILBERTA_EUNSUPPORTED, "tile %d does not divide %lld image tokens", c->tile,
                     (long long)n_img);
     if (c->delta < 0) return fail(HILBERTA_EINVAL, "delta %d < 0", c->delta);
@@ -63,16 +65,43 @@ int check_config(const hilberta_config* c) {
     if (c->shared_h + c->shared_w > 255)
         return fail(HILBERTA_EUNSUPPORTED, "shared region %dx%d: shared_h + shared_w must be <= 255",
                     c->shared_h, c->shared_w);
+    if (c->layout == HILBERTA_LAYOUT_MOVED) {
+        const int64_t tiled = n_img - (int64_t)c->shared_h * c->shared_w;
+        if (tiled < 1 || tiled % c->tile)
+            return fail(HILBERTA_EUNSUPPORTED, "tile %d does not divide the %lld tokens outside the shared region",
+                        c->tile, (long long)tiled);
+    }
     return HILBERTA_OK;
 }
 
-int64_t span_capacity(const hilberta_config* c) {
-    return c->shared_h * c->shared_w ? c->shared_h + c->shared_w + 1 : 0;
+// The sequence a valid config describes: in place, all N_img image tokens
+// are tiled and the shared ones keep their slots; moved, the shared tokens
+// follow the text in the global prefix and the other N_img - N_sh are tiled.
+struct Geom {
+    int64_t prefix, tiled, shared_in_span, cap;
+};
+
+Geom geom(const hilberta_config* c) {
+    const int64_t n_img = (int64_t)c->grid_h * c->grid_w;
+    const int64_t n_sh = (int64_t)c->shared_h * c->shared_w;
+    Geom g{};
+    if (c->layout == HILBERTA_LAYOUT_MOVED) {
+        g.prefix = c->n_txt + n_sh;
+        g.tiled = n_img - n_sh;
+        g.shared_in_span = 0;
+        g.cap = 0;
+    } else {
+        g.prefix = c->n_txt;
+        g.tiled = n_img;
+        g.shared_in_span = n_sh;
+        g.cap = n_sh ? c->shared_h + c->shared_w + 1 : 0;
+    }
+    return g;
 }
 
 int64_t schedule_words(const hilberta_config* c) {
-    const int64_t n_img = (int64_t)c->grid_h * c->grid_w;
-    return 12 + 4 * (n_img / c->tile) + 2 * span_capacity(c);
+    const Geom g = geom(c);
+    return 12 + 4 * (g.tiled / c->tile) + 2 * g.cap;
 }
 
 struct Tensor4 {
@@ -170,14 +199,16 @@ int run_attention(bool sparse, const hilberta_config* cfg, const int32_t* sched,
     if (ws_bytes < 0 || (ws == nullptr && ws_bytes != 0))
         return fail(HILBERTA_EINVAL, "workspace NULL with %lld bytes", (long long)ws_bytes);
     if (ws && (uintptr_t)ws % 16) return fail(HILBERTA_EUNSUPPORTED, "workspace is not 16-byte aligned");
+    // the attention sees a global prefix and a tiled span (see Geom)
     int64_t n_txt = 0, n_img = n_tot, n_shared = 0, tile = n_tot, n_tiles = 1, cap = 0;
     if (sparse) {
-        n_txt = cfg->n_txt;
-        n_img = (int64_t)cfg->grid_h * cfg->grid_w;
-        n_shared = (int64_t)cfg->shared_h * cfg->shared_w;
+        const Geom g = geom(cfg);
+        n_txt = g.prefix;
+        n_img = g.tiled;
+        n_shared = g.shared_in_span;
         tile = cfg->tile;
         n_tiles = n_img / tile;
-        cap = span_capacity(cfg);
+        cap = g.cap;
     }
     if (n_tot > 0x7fffffffLL) return fail(HILBERTA_EUNSUPPORTED, "sequence too long");
     {
@@ -295,6 +326,19 @@ int hilberta_build_perm(int32_t grid_h, int32_t grid_w, int32_t* perm, int32_t* 
                       "build_perm launch");
 }
 
+int hilberta_build_perm_layout(const hilberta_config* cfg, int32_t* perm, int32_t* inv_or_null,
+                               void* stream) {
+    int rc = check_config(cfg);
+    if (rc) return rc;
+    if (!perm) return fail(HILBERTA_EINVAL, "perm is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (cfg->layout == HILBERTA_LAYOUT_MOVED && cfg->shared_h * cfg->shared_w > 0)
+        return hip_status(hilberta::launch_build_perm_moved(cfg->grid_w, cfg->shared_h, cfg->shared_w, perm,
+                                                            inv_or_null, s),
+                          "build_perm launch");
+    return hip_status(hilberta::launch_build_perm(cfg->grid_w, perm, inv_or_null, s), "build_perm launch");
+}
+
 int hilberta_permute(const void* x, void* y, const int32_t* perm, int64_t batch, int64_t n,
                      int64_t channels, int64_t x_batch_stride, int64_t x_row_stride,
                      int64_t y_batch_stride, int64_t y_row_stride, int dtype, void* stream) {
@@ -328,19 +372,22 @@ int hilberta_schedule(const hilberta_config* cfg, int32_t layer, int32_t* sched,
     if (capacity < words)
         return fail(HILBERTA_ECAPACITY, "schedule needs %lld words, capacity %lld", (long long)words,
                     (long long)capacity);
-    const int64_t n_img = (int64_t)cfg->grid_h * cfg->grid_w;
+    const Geom g = geom(cfg);
     hilberta::ScheduleArgs a{};
     a.out = sched;
     a.grid_h = cfg->grid_h;
     a.grid_w = cfg->grid_w;
     a.n_txt = cfg->n_txt;
     a.tile = cfg->tile;
-    a.n_tiles = (int32_t)(n_img / cfg->tile);
+    a.n_tiles = (int32_t)(g.tiled / cfg->tile);
     a.shared_h = cfg->shared_h;
     a.shared_w = cfg->shared_w;
+    a.prefix = (int32_t)g.prefix;
+    a.tiled = (int32_t)g.tiled;
+    a.moved = cfg->layout == HILBERTA_LAYOUT_MOVED;
     a.layer = layer;
-    a.offset = (int32_t)(((int64_t)layer * cfg->delta) % n_img);
-    a.span_cap = (int32_t)span_capacity(cfg);
+    a.offset = (int32_t)(((int64_t)layer * cfg->delta) % g.tiled);
+    a.span_cap = (int32_t)g.cap;
     a.words = (int32_t)words;
     return hip_status(hilberta::launch_schedule(a, static_cast<hipStream_t>(stream)), "schedule launch");
 }
@@ -354,10 +401,10 @@ int hilberta_attn_workspace_bytes(const hilberta_config* cfg, int64_t batch, int
     if (head_dim != 64 && head_dim != 128)
         return fail(HILBERTA_EUNSUPPORTED, "head_dim %lld not in {64, 128}", (long long)head_dim);
     if (dtype != HILBERTA_F32 && dtype != HILBERTA_BF16) return fail(HILBERTA_EUNSUPPORTED, "dtype %d", dtype);
-    const int64_t n_img = (int64_t)cfg->grid_h * cfg->grid_w;
-    const int64_t n_tot = cfg->n_txt + n_img;
-    const Plan p = make_plan(true, cfg->n_txt, n_img, (int64_t)cfg->shared_h * cfg->shared_w,
-                             cfg->tile, n_tot, batch * heads, head_dim, dtype, true);
+    const Geom g = geom(cfg);
+    const int64_t n_tot = cfg->n_txt + (int64_t)cfg->grid_h * cfg->grid_w;
+    const Plan p = make_plan(true, g.prefix, g.tiled, g.shared_in_span, cfg->tile, n_tot, batch * heads,
+                             head_dim, dtype, true);
     *bytes = p.ws_bytes;
     return HILBERTA_OK;
 }

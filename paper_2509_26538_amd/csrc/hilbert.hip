@@ -74,60 +74,75 @@ __global__ void __launch_bounds__(256) build_perm_kernel(int32_t side, int32_t* 
 // Shared runs: every cell of the central region finds its Hilbert position d
 // and whether it starts a run (d-1 lies outside the region, or d = 0) or ends
 // one (d+1 outside, or d = N-1).  Starts and ends are ranked separately; the
-// i-th start pairs with the i-th end.  One workgroup; also writes the header.
-__global__ void __launch_bounds__(256) shared_runs_kernel(ScheduleArgs a) {
-    __shared__ int32_t starts[kMaxSpans];
-    __shared__ int32_t ends[kMaxSpans];
-    __shared__ int32_t sorted_starts[kMaxSpans];
-    __shared__ int32_t sorted_ends[kMaxSpans];
-    __shared__ int32_t n_starts, n_ends;
+// i-th start pairs with the i-th end.  The whole workgroup calls this; the
+// sorted run starts and (inclusive) ends land in LDS; returns the run count.
+struct RunsLds {
+    int32_t starts[kMaxSpans];
+    int32_t ends[kMaxSpans];
+    int32_t sorted_starts[kMaxSpans];
+    int32_t sorted_ends[kMaxSpans];
+    int32_t n_starts, n_ends;
+};
+
+__device__ int32_t shared_runs(RunsLds& r, int32_t side, int32_t shared_h, int32_t shared_w,
+                               int32_t cap) {
     const int tid = threadIdx.x;
-    const int order = log2_side(a.grid_w);
-    const uint32_t n_img = (uint32_t)a.grid_h * (uint32_t)a.grid_w;
-    const int32_t r0 = (a.grid_h - a.shared_h) / 2;
-    const int32_t c0 = (a.grid_w - a.shared_w) / 2;
-    const int32_t n_cells = a.shared_h * a.shared_w;
+    const int order = log2_side(side);
+    const uint32_t n_img = (uint32_t)side * (uint32_t)side;
+    const int32_t r0 = (side - shared_h) / 2;
+    const int32_t c0 = (side - shared_w) / 2;
+    const int32_t n_cells = shared_h * shared_w;
     if (tid == 0) {
-        n_starts = 0;
-        n_ends = 0;
+        r.n_starts = 0;
+        r.n_ends = 0;
     }
     __syncthreads();
     auto inside = [&](uint32_t d) {
         uint32_t x, y;
         hilbert_d2xy(order, d, x, y);
-        return (int32_t)y >= r0 && (int32_t)y < r0 + a.shared_h && (int32_t)x >= c0 &&
-               (int32_t)x < c0 + a.shared_w;
+        return (int32_t)y >= r0 && (int32_t)y < r0 + shared_h && (int32_t)x >= c0 &&
+               (int32_t)x < c0 + shared_w;
     };
     for (int32_t u = tid; u < n_cells; u += blockDim.x) {
-        const uint32_t y = (uint32_t)(r0 + u / a.shared_w);
-        const uint32_t x = (uint32_t)(c0 + u % a.shared_w);
+        const uint32_t y = (uint32_t)(r0 + u / shared_w);
+        const uint32_t x = (uint32_t)(c0 + u % shared_w);
         const uint32_t d = hilbert_xy2d(order, x, y);
         if (d == 0 || !inside(d - 1)) {
-            const int32_t i = atomicAdd(&n_starts, 1);
-            if (i < kMaxSpans) starts[i] = (int32_t)d;
+            const int32_t i = atomicAdd(&r.n_starts, 1);
+            if (i < kMaxSpans) r.starts[i] = (int32_t)d;
         }
         if (d == n_img - 1 || !inside(d + 1)) {
-            const int32_t i = atomicAdd(&n_ends, 1);
-            if (i < kMaxSpans) ends[i] = (int32_t)d;
+            const int32_t i = atomicAdd(&r.n_ends, 1);
+            if (i < kMaxSpans) r.ends[i] = (int32_t)d;
         }
     }
     __syncthreads();
-    int32_t n_runs = min(min(n_starts, n_ends), a.span_cap);
+    int32_t n_runs = min(min(r.n_starts, r.n_ends), cap);
     n_runs = min(n_runs, kMaxSpans);
     for (int32_t i = tid; i < n_runs; i += blockDim.x) {
         int32_t rank_s = 0, rank_e = 0;
         for (int32_t j = 0; j < n_runs; ++j) {
-            rank_s += starts[j] < starts[i];
-            rank_e += ends[j] < ends[i];
+            rank_s += r.starts[j] < r.starts[i];
+            rank_e += r.ends[j] < r.ends[i];
         }
-        sorted_starts[rank_s] = starts[i];
-        sorted_ends[rank_e] = ends[i];
+        r.sorted_starts[rank_s] = r.starts[i];
+        r.sorted_ends[rank_e] = r.ends[i];
     }
     __syncthreads();
+    return n_runs;
+}
+
+// The schedule's header and shared runs (none in the moved-prefix layout,
+// where the shared tokens sit in the prefix).  One workgroup.
+__global__ void __launch_bounds__(256) shared_runs_kernel(ScheduleArgs a) {
+    __shared__ RunsLds r;
+    const int tid = threadIdx.x;
+    const int32_t n_cells = a.shared_h * a.shared_w;
+    const int32_t n_runs = a.moved || n_cells == 0 ? 0 : shared_runs(r, a.grid_w, a.shared_h, a.shared_w, a.span_cap);
     int32_t* spans = a.out + 12 + 4 * a.n_tiles;
     for (int32_t i = tid; i < n_runs; i += blockDim.x) {
-        spans[2 * i] = a.n_txt + sorted_starts[i];
-        spans[2 * i + 1] = sorted_ends[i] + 1 - sorted_starts[i];
+        spans[2 * i] = a.prefix + r.sorted_starts[i];
+        spans[2 * i + 1] = r.sorted_ends[i] + 1 - r.sorted_starts[i];
     }
     for (int32_t i = n_runs + tid; i < a.span_cap; i += blockDim.x) {
         spans[2 * i] = 0;
@@ -136,8 +151,8 @@ __global__ void __launch_bounds__(256) shared_runs_kernel(ScheduleArgs a) {
     if (tid == 0) {
         int32_t* h = a.out;
         h[0] = 0x48424131;
-        h[1] = a.n_txt;
-        h[2] = (int32_t)n_img;
+        h[1] = a.prefix;
+        h[2] = a.tiled;
         h[3] = a.tile;
         h[4] = a.n_tiles;
         h[5] = a.offset;
@@ -150,14 +165,44 @@ __global__ void __launch_bounds__(256) shared_runs_kernel(ScheduleArgs a) {
     }
 }
 
-// Tiles of the slid partition: tile q holds the image positions p with
-// floor(((p + o) mod N_img) / N_T) = q, i.e. the cyclic range that starts at
-// (q N_T - o) mod N_img.  Reads the runs written by shared_runs_kernel to
-// count the shared tokens inside each tile.
+// The moved-prefix order of the image tokens: the shared tokens first, then
+// the others, each part in Hilbert order.  Hilbert position d goes to slot
+// c(d) if its cell is shared, else N_sh + d - c(d), where c(d) counts the
+// shared cells at Hilbert positions below d (from the shared runs, which
+// every workgroup finds for itself).
+__global__ void __launch_bounds__(256) build_perm_moved_kernel(int32_t side, int32_t shared_h, int32_t shared_w,
+                                                               int32_t* __restrict__ perm,
+                                                               int32_t* __restrict__ inv) {
+    __shared__ RunsLds r;
+    const int32_t n_runs = shared_runs(r, side, shared_h, shared_w, kMaxSpans);
+    const int order = log2_side(side);
+    const uint32_t n = (uint32_t)side * (uint32_t)side;
+    const int32_t n_sh = shared_h * shared_w;
+    for (uint32_t d = blockIdx.x * blockDim.x + threadIdx.x; d < n; d += gridDim.x * blockDim.x) {
+        int32_t below = 0;
+        bool shared = false;
+        for (int32_t i = 0; i < n_runs; ++i) {
+            const int32_t st = r.sorted_starts[i], en = r.sorted_ends[i];
+            below += max(0, min((int32_t)d, en + 1) - st);
+            shared |= (int32_t)d >= st && (int32_t)d <= en;
+        }
+        uint32_t x, y;
+        hilbert_d2xy(order, d, x, y);
+        const uint32_t raster = y * (uint32_t)side + x;
+        const int32_t slot = shared ? below : n_sh + (int32_t)d - below;
+        perm[slot] = (int32_t)raster;
+        if (inv) inv[raster] = slot;
+    }
+}
+
+// Tiles of the slid partition: tile q holds the positions p of the tiled
+// span (N tokens) with floor(((p + o) mod N) / N_T) = q, i.e. the cyclic range
+// that starts at (q N_T - o) mod N.  Reads the runs written by
+// shared_runs_kernel to count the shared tokens inside each tile.
 __global__ void __launch_bounds__(256) tiles_kernel(ScheduleArgs a) {
     const int32_t q = blockIdx.x * blockDim.x + threadIdx.x;
     if (q >= a.n_tiles) return;
-    const int32_t n_img = a.grid_h * a.grid_w;
+    const int32_t n_img = a.tiled;
     const int32_t start = (int32_t)(((int64_t)q * a.tile - a.offset + n_img) % n_img);
     const int32_t len1 = min(a.tile, n_img - start);
     const int32_t len2 = a.tile - len1;
@@ -165,13 +210,13 @@ __global__ void __launch_bounds__(256) tiles_kernel(ScheduleArgs a) {
     const int32_t n_runs = a.out[6];
     int32_t ns = 0;
     for (int32_t s = 0; s < n_runs; ++s) {
-        const int32_t lo = spans[2 * s] - a.n_txt;
+        const int32_t lo = spans[2 * s] - a.prefix;
         const int32_t hi = lo + spans[2 * s + 1];
         ns += max(0, min(hi, start + len1) - max(lo, start));
         ns += max(0, min(hi, len2) - max(lo, 0));
     }
     int32_t* t = a.out + 12 + 4 * q;
-    t[0] = a.n_txt + start;
+    t[0] = a.prefix + start;
     t[1] = len1;
     t[2] = len2;
     t[3] = ns;
@@ -184,6 +229,16 @@ hipError_t launch_build_perm(int32_t side, int32_t* perm, int32_t* inv, hipStrea
     const int64_t want = (n + 255) / 256;
     const int blocks = (int)(want < 65536 ? want : 65536);
     hipLaunchKernelGGL(build_perm_kernel, dim3(blocks), dim3(256), 0, s, side, perm, inv);
+    return hipGetLastError();
+}
+
+hipError_t launch_build_perm_moved(int32_t side, int32_t shared_h, int32_t shared_w, int32_t* perm,
+                                   int32_t* inv, hipStream_t s) {
+    const int64_t n = (int64_t)side * side;
+    const int64_t want = (n + 255) / 256;
+    // every workgroup first finds the shared runs: keep the grid moderate
+    const int blocks = (int)(want < 1024 ? want : 1024);
+    hipLaunchKernelGGL(build_perm_moved_kernel, dim3(blocks), dim3(256), 0, s, side, shared_h, shared_w, perm, inv);
     return hipGetLastError();
 }
 

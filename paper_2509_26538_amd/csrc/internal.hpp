@@ -78,12 +78,17 @@ hipError_t launch_merge(const MergeArgs& m, int dtype, int head_dim, hipStream_t
 
 // ----------------------------------------------------- permutation, schedule
 hipError_t launch_build_perm(int32_t side, int32_t* perm, int32_t* inv, hipStream_t s);
+hipError_t launch_build_perm_moved(int32_t side, int32_t shared_h, int32_t shared_w, int32_t* perm,
+                                   int32_t* inv, hipStream_t s);
 
 struct ScheduleArgs {
     int32_t* out;
     int32_t grid_h, grid_w, n_txt, tile, n_tiles, shared_h, shared_w;
+    int32_t prefix;     // global prefix: n_txt, plus the shared tokens when moved
+    int32_t tiled;      // tokens of the tiled span: N_img, or N_img - N_sh when moved
+    int32_t moved;      // 1: shared tokens gathered next to the text
     int32_t layer;
-    int32_t offset;     // (layer * delta) mod N_img, computed on the host in 64 bits
+    int32_t offset;     // (layer * delta) mod tiled, computed on the host in 64 bits
     int32_t span_cap;
     int32_t words;
 };

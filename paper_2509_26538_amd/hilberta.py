@@ -18,11 +18,14 @@ HILBERTA_EHIP = -4
 HILBERTA_F32 = 0
 HILBERTA_BF16 = 1
 SCHEDULE_MAGIC = 0x48424131
+LAYOUT_IN_PLACE = 0
+LAYOUT_MOVED = 1
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhilberta.so")
 
 EXPORTS = [
-    "hilberta_version", "hilberta_last_error", "hilberta_build_perm", "hilberta_permute",
+    "hilberta_version", "hilberta_last_error", "hilberta_build_perm",
+    "hilberta_build_perm_layout", "hilberta_permute",
     "hilberta_unpermute", "hilberta_schedule_words", "hilberta_schedule",
     "hilberta_attn_workspace_bytes", "hilberta_attn_fwd", "dense_attn_workspace_bytes",
     "dense_attn_fwd",
@@ -31,7 +34,8 @@ EXPORTS = [
 
 class hilberta_config(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in
-                ("grid_h", "grid_w", "n_txt", "tile", "delta", "shared_h", "shared_w")]
+                ("grid_h", "grid_w", "n_txt", "tile", "delta", "shared_h", "shared_w",
+                 "layout")]
 
 
 class HilbertaError(RuntimeError):
@@ -62,6 +66,7 @@ def load(path=LIB_PATH):
         "hilberta_version": (ctypes.c_int, []),
         "hilberta_last_error": (ctypes.c_char_p, []),
         "hilberta_build_perm": (ctypes.c_int, [_I32, _I32, _P, _P, _P]),
+        "hilberta_build_perm_layout": (ctypes.c_int, [_CFGP, _P, _P, _P]),
         "hilberta_permute": (ctypes.c_int, [_P, _P, _P] + [_I64] * 7 + [ctypes.c_int, _P]),
         "hilberta_unpermute": (ctypes.c_int, [_P, _P, _P] + [_I64] * 7 + [ctypes.c_int, _P]),
         "hilberta_schedule_words": (ctypes.c_int, [_CFGP, _I64P]),
@@ -119,11 +124,11 @@ def _dtype(t):
     raise HilbertaError(HILBERTA_EUNSUPPORTED, "dtype %s" % t.dtype)
 
 
-def make_config(grid, n_txt, tile, delta, shared_h=0, shared_w=None):
+def make_config(grid, n_txt, tile, delta, shared_h=0, shared_w=None, layout=LAYOUT_IN_PLACE):
     """hilberta_config for a grid x grid latent grid."""
     if shared_w is None:
         shared_w = shared_h
-    return hilberta_config(grid, grid, n_txt, tile, delta, shared_h, shared_w)
+    return hilberta_config(grid, grid, n_txt, tile, delta, shared_h, shared_w, layout)
 
 
 def hilberta_version():
@@ -132,6 +137,11 @@ def hilberta_version():
 
 def hilberta_build_perm(grid_h, grid_w, perm, inv=None, stream=None):
     _check(load().hilberta_build_perm(grid_h, grid_w, _ptr(perm), _ptr(inv), _stream(stream)))
+
+
+def hilberta_build_perm_layout(cfg, perm, inv=None, stream=None):
+    _check(load().hilberta_build_perm_layout(ctypes.byref(cfg), _ptr(perm), _ptr(inv),
+                                             _stream(stream)))
 
 
 def _permute(name, x, y, perm, stream):

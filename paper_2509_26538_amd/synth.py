@@ -31,6 +31,7 @@ class Workload:
     layers: tuple = (0,)
     hidden: int = 3072    # hidden size of the token gather workload
     seed: int = 0
+    moved: bool = False   # shared tokens gathered next to the text (Appendix A)
 
     @property
     def n_img(self):
@@ -61,6 +62,12 @@ WORKLOADS = {
     "table1-64-g16": Workload("table1-64-g16", 64, 512, 1, 24, 128, "bf16", 256, 64, 16),
     "table1-128-g4": Workload("table1-128-g4", 128, 512, 1, 24, 128, "bf16", 4096, 1024, 32),
     "table1-128-g16": Workload("table1-128-g16", 128, 512, 1, 24, 128, "bf16", 1024, 256, 32),
+    # the same settings in the moved-prefix layout of Appendix A: the shared
+    # tokens follow the text and the other N_img - N_sh tokens form G tiles
+    "moved-64-g4": Workload("moved-64-g4", 64, 512, 1, 24, 128, "bf16", 960, 240, 16, moved=True),
+    "moved-64-g16": Workload("moved-64-g16", 64, 512, 1, 24, 128, "bf16", 240, 60, 16, moved=True),
+    "moved-128-g4": Workload("moved-128-g4", 128, 512, 1, 24, 128, "bf16", 3840, 960, 32, moved=True),
+    "moved-128-g16": Workload("moved-128-g16", 128, 512, 1, 24, 128, "bf16", 960, 240, 32, moved=True),
 }
 
 

@@ -18,11 +18,12 @@ BF16_MEAN_ABS = 1e-3
 
 def config_of(layout):
     return hb.hilberta_config(layout.grid_h, layout.grid_w, layout.n_txt, layout.tile,
-                              layout.delta, layout.shared_h, layout.shared_w)
+                              layout.delta, layout.shared_h, layout.shared_w,
+                              hb.LAYOUT_MOVED if layout.moved else hb.LAYOUT_IN_PLACE)
 
 
 def layout_of(w):
-    return Layout(w.grid, w.grid, w.n_txt, w.tile, w.delta, w.shared, w.shared)
+    return Layout(w.grid, w.grid, w.n_txt, w.tile, w.delta, w.shared, w.shared, moved=w.moved)
 
 
 def make_schedule(layout, layer, dev):

@@ -63,6 +63,12 @@ BAD_CONFIGS = [
     (hb.hilberta_config(8, 8, 0, 16, 2, 2, 0), hb.HILBERTA_EINVAL),          # half a region
     (hb.hilberta_config(256, 256, 0, 256, 2, 200, 100), hb.HILBERTA_EUNSUPPORTED),  # too many runs
     (hb.hilberta_config(32768, 32768, 2 ** 30, 1024, 2, 0, 0), hb.HILBERTA_EUNSUPPORTED),  # too long
+    (hb.hilberta_config(8, 8, 0, 16, 2, 0, 0, 2), hb.HILBERTA_EINVAL),       # unknown layout
+    (hb.hilberta_config(8, 8, 0, 16, 2, 0, 0, -1), hb.HILBERTA_EINVAL),      # unknown layout
+    # moved: the tile must divide the 60 tokens outside a 2x2 region, not the 64
+    (hb.hilberta_config(8, 8, 0, 16, 2, 2, 2, hb.LAYOUT_MOVED), hb.HILBERTA_EUNSUPPORTED),
+    # moved: a region that covers the grid leaves nothing to tile
+    (hb.hilberta_config(8, 8, 0, 1, 2, 8, 8, hb.LAYOUT_MOVED), hb.HILBERTA_EUNSUPPORTED),
 ]
 
 
@@ -78,11 +84,33 @@ def test_schedule_rejects_bad_configs(lib, cfg, rc):
                                     osched.Layout(64, 64, 512, 256, 128, 8, 8),
                                     osched.Layout(8, 8, 3, 16, 5, 3, 2),
                                     osched.Layout(128, 128, 512, 1024, 512, 16, 16),
-                                    osched.Layout(4, 4, 0, 16, 3, 0, 0)])
+                                    osched.Layout(4, 4, 0, 16, 3, 0, 0),
+                                    osched.Layout(16, 16, 0, 60, 15, 4, 4, moved=True),
+                                    osched.Layout(8, 8, 3, 15, 4, 2, 2, moved=True),
+                                    osched.Layout(64, 64, 512, 1023, 341, 2, 2, moved=True),
+                                    osched.Layout(16, 16, 5, 64, 16, moved=True)])
 def test_schedule_words_match_documented_layout(layout):
     cfg = hb.hilberta_config(layout.grid_h, layout.grid_w, layout.n_txt, layout.tile,
-                             layout.delta, layout.shared_h, layout.shared_w)
+                             layout.delta, layout.shared_h, layout.shared_w, int(layout.moved))
     assert hb.hilberta_schedule_words(cfg) == osched.table_words(layout)
+
+
+def test_moved_tile_need_not_divide_the_image(lib):
+    # 60 = 64 - 2*2 tokens outside the region: tiles of 15 are valid moved, not in place
+    moved = hb.hilberta_config(8, 8, 0, 15, 2, 2, 2, hb.LAYOUT_MOVED)
+    assert hb.hilberta_schedule_words(moved) == 12 + 4 * 4
+    in_place = hb.hilberta_config(8, 8, 0, 15, 2, 2, 2, hb.LAYOUT_IN_PLACE)
+    w = ctypes.c_int64(0)
+    assert lib.hilberta_schedule_words(ctypes.byref(in_place), ctypes.byref(w)) == hb.HILBERTA_EUNSUPPORTED
+
+
+def test_build_perm_layout_errors(lib):
+    cfg = hb.make_config(8, 0, 15, 2, 2, layout=hb.LAYOUT_MOVED)
+    assert lib.hilberta_build_perm_layout(ctypes.byref(cfg), None, None, None) == hb.HILBERTA_EINVAL
+    assert "perm" in hb.last_error()
+    assert lib.hilberta_build_perm_layout(None, FAKE, None, None) == hb.HILBERTA_EINVAL
+    for cfg, rc in BAD_CONFIGS:
+        assert lib.hilberta_build_perm_layout(ctypes.byref(cfg), FAKE, None, None) == rc
 
 
 def test_schedule_capacity_and_layer_errors(lib):

@@ -18,6 +18,7 @@ from oracle.schedule import Layout
 import test_oracle_accounting as t_acc
 import test_oracle_attention as t_att
 import test_oracle_hilbert as t_hil
+import test_oracle_moved as t_mov
 import test_oracle_schedule as t_sch
 import test_oracle_tokens as t_tok
 
@@ -45,6 +46,10 @@ PINS = [
     lambda: t_tok.test_gather_orders_tokens_along_the_curve(8),
     lambda: t_tok.test_scatter_restores_raster_order(4),
     lambda: t_acc.test_nnz_matches_closed_form(Layout(16, 16, 0, 64, 32, 4, 4), 1, 22_368),
+    lambda: t_mov.test_moved_order_is_shared_first_then_hilbert(t_mov.MOVED[1]),
+    lambda: t_mov.test_tiles_partition_the_tiled_span(t_mov.MOVED[0], 1),
+    lambda: t_mov.test_moved_sequence_equals_raster_construction(t_mov.MOVED[2], 1),
+    lambda: t_mov.test_pattern_size_closed_form(t_mov.MOVED[3]),
 ]
 
 
@@ -154,6 +159,17 @@ def _nnz_drops_last_block(orig):
     return f
 
 
+def _moved_is_the_plain_curve(orig):
+    return lambda layout: hilbert.build_perm(layout.grid_h, layout.grid_w)[0]
+
+
+def _moved_parts_in_raster_order(orig):
+    def f(layout):
+        sh = schedule.shared_raster(layout)
+        return np.concatenate([np.nonzero(sh)[0], np.nonzero(~sh)[0]])
+    return f
+
+
 MUTANTS = {
     "curve transposed": (hilbert, "xy_iterative", _xy_transposed),
     "curve without reflection": (hilbert, "xy_iterative", _xy_no_reflection),
@@ -169,6 +185,10 @@ MUTANTS = {
     "lse without the max": (attention, "masked_attention", _attention_with("lse_without_max")),
     "gather through the inverse": (tokens, "permute", _permute_through_inverse),
     "nnz drops the last row": (accounting, "nnz", _nnz_drops_last_block),
+    "moved order is the plain curve": (schedule, "moved_perm", _moved_is_the_plain_curve),
+    "moved parts in raster order": (schedule, "moved_perm", _moved_parts_in_raster_order),
+    "moved prefix without the shared tokens": (
+        Layout, "prefix", lambda orig: property(lambda self: self.n_txt)),
 }
 
 
