@@ -194,3 +194,28 @@ def test_runs_reproduce_the_shared_set_and_are_maximal(side):
             assert np.array_equal(back, flags)
             ends = [s + ln for s, ln in r]
             assert all(e < s2 for e, (s2, _) in zip(ends, r[1:]))  # a gap between runs
+
+
+@pytest.mark.parametrize("g", [4, 16])
+def test_slide_direction_at_a_quarter_tile(g):
+    # With the paper's slide cycle of 4 (Delta = N_T/4) the direction of the
+    # slide is observable: the label formula of §3.2 puts the boundaries at
+    # q N_T - o, so at layer 1 tile 0 starts a quarter tile before the end of
+    # the sequence and wraps.  A window that moved the other way would put
+    # them at q N_T + o; over one slide cycle both visit the same partitions,
+    # layer l of one being layer (4 - l) mod 4 of the other.
+    layout = Layout(64, 64, 0, 4096 // g, 1024 // g, 0, 0)
+    n, nt = layout.n_img, layout.tile
+    p = np.arange(n)
+    t = schedule.schedule_table(layout, 1)
+    assert t[12] == n - nt // 4 and t[13] == nt // 4 and t[14] == nt - nt // 4
+    for layer in range(4):
+        lab = schedule.labels(layout, layer)
+        o = (layer * layout.delta) % n
+        assert np.array_equal(lab, ((p + o) // nt) % g)
+        other = ((p - ((4 - layer) % 4) * layout.delta) % n) // nt
+        same = lab[:, None] == lab[None, :]
+        assert np.array_equal(same, other[:, None] == other[None, :])
+        if layer % 2:
+            forward = ((p - o) % n) // nt
+            assert not np.array_equal(same, forward[:, None] == forward[None, :])
