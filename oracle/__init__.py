@@ -9,7 +9,9 @@ Everything here is slow and obviously correct on purpose:
 
 * ``hilbert``    -- the Hilbert linearisation pi of a 2^k x 2^k grid (§3.1),
                     built twice, by the iterative bit-pair algorithm and by an
-                    L-system turtle, so that each pins the other.
+                    L-system turtle, so that each pins the other; other grid
+                    shapes embedded in their enclosing 2^k square with padding
+                    (Appendix D).
 * ``schedule``   -- tile labels, sliding offsets, the central shared region,
                     the explicit 0/1 attention mask (§3.2, §3.3, Appendix A)
                     and the schedule table in the library's documented layout.

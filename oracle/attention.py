@@ -25,12 +25,14 @@ def _as_f64(x):
     return np.asarray(x, dtype=np.float64)
 
 
-def masked_attention(q, k, v, mask_fn, scale=None, block=1024):
+def masked_attention(q, k, v, mask_fn, scale=None, block=1024, empty_rows=False):
     """O and LSE for q, k, v of shape [B, H, N, D] (any float dtype, upcast).
 
     ``mask_fn(rows)`` returns the bool mask rows [len(rows), N]; the same mask
     applies to every batch entry and head.  Returns float64 (O [B,H,N,D],
-    LSE [B,H,N]).
+    LSE [B,H,N]).  A row that attends no key is an error unless
+    ``empty_rows`` is set: then it is an empty softmax, O = 0 and LSE = -inf
+    (the padding rows of a general shape).
     """
     q, k, v = _as_f64(q), _as_f64(k), _as_f64(v)
     b, h, n, d = q.shape
@@ -41,15 +43,20 @@ def masked_attention(q, k, v, mask_fn, scale=None, block=1024):
     for r0 in range(0, n, block):
         rows = np.arange(r0, min(n, r0 + block))
         m = mask_fn(rows)
-        if not m.any(axis=1).all():
+        some = m.any(axis=1)
+        if not some.all() and not empty_rows:
             raise ValueError("every row must attend at least one key")
         s = np.einsum("bhid,bhjd->bhij", q[:, :, rows], k) * scale
         s = np.where(m[None, None], s, -np.inf)
         mx = s.max(axis=-1, keepdims=True)
+        mx = np.where(some[None, None, :, None], mx, 0.0)
         p = np.exp(s - mx)
         den = p.sum(axis=-1, keepdims=True)
-        out[:, :, rows] = np.einsum("bhij,bhjd->bhid", p, v) / den
-        lse[:, :, rows] = (mx + np.log(den))[..., 0]
+        with np.errstate(divide="ignore", invalid="ignore"):
+            o = np.einsum("bhij,bhjd->bhid", p, v) / den
+            ls = (mx + np.log(den))[..., 0]
+        out[:, :, rows] = np.where(some[None, None, :, None], o, 0.0)
+        lse[:, :, rows] = np.where(some[None, None, :], ls, -np.inf)
     return out, lse
 
 
@@ -64,12 +71,18 @@ def masked_attention_rows(q, k, v, rows, mask_rows, scale=None):
     if scale is None:
         scale = 1.0 / math.sqrt(d)
     rows = np.asarray(rows, dtype=np.int64)
+    some = np.asarray(mask_rows).any(axis=1)
     s = np.einsum("bhid,bhjd->bhij", q[:, :, rows], k) * scale
     s = np.where(mask_rows[None, None], s, -np.inf)
     mx = s.max(axis=-1, keepdims=True)
+    mx = np.where(some[None, None, :, None], mx, 0.0)
     p = np.exp(s - mx)
     den = p.sum(axis=-1, keepdims=True)
-    return np.einsum("bhij,bhjd->bhid", p, v) / den, (mx + np.log(den))[..., 0]
+    with np.errstate(divide="ignore", invalid="ignore"):
+        o = np.einsum("bhij,bhjd->bhid", p, v) / den
+        ls = (mx + np.log(den))[..., 0]
+    return (np.where(some[None, None, :, None], o, 0.0),
+            np.where(some[None, None, :], ls, -np.inf))
 
 
 def dense_attention(q, k, v, scale=None, block=1024):

@@ -102,8 +102,8 @@ def order_of(side):
 def build_perm(grid_h, grid_w):
     """perm[d] = raster index (y*W + x) of Hilbert position d, and its inverse.
 
-    Only square power-of-two grids have a Hilbert curve (§3.1; Appendix D
-    embeds other shapes in an enclosing grid, which this oracle does not do).
+    Only square power-of-two grids have a Hilbert curve (§3.1); other shapes
+    go through ``padded_perm``.
     """
     if grid_h != grid_w:
         raise ValueError("the Hilbert order needs a square grid")
@@ -112,4 +112,34 @@ def build_perm(grid_h, grid_w):
     perm = (y * grid_w + x).astype(np.int64)
     inv = np.empty_like(perm)
     inv[perm] = np.arange(perm.size, dtype=np.int64)
+    return perm, inv
+
+
+def enclosing_side(grid_h, grid_w):
+    """Side of the smallest power-of-two square, at least 2 x 2, that holds
+    a grid_h x grid_w grid: the "even-sized" grid Appendix D builds the curve
+    over for a general shape (read as the next power of two per side, made
+    square, since the curve needs a 2^k square)."""
+    if grid_h < 1 or grid_w < 1:
+        raise ValueError("empty grid %dx%d" % (grid_h, grid_w))
+    side = 2
+    while side < max(grid_h, grid_w):
+        side *= 2
+    return side
+
+
+def padded_perm(grid_h, grid_w):
+    """The Hilbert order of a grid_h x grid_w grid embedded in its enclosing
+    S x S grid (Appendix D): perm[d], for the S*S positions d of the
+    enclosing curve, is the raster index y*grid_w + x of the cell (x, y) at
+    position d when that cell lies inside the grid, and -1 when it is
+    padding; inv[y*grid_w + x] = d for the grid's own cells.  The cell at
+    the grid's origin is the enclosing grid's origin.
+    """
+    side = enclosing_side(grid_h, grid_w)
+    x, y = xy_iterative(order_of(side))
+    inside = (x < grid_w) & (y < grid_h)
+    perm = np.where(inside, y * grid_w + x, -1).astype(np.int64)
+    inv = np.empty(grid_h * grid_w, dtype=np.int64)
+    inv[perm[inside]] = np.nonzero(inside)[0]
     return perm, inv

@@ -25,6 +25,15 @@ instead: the shared tokens are gathered next to the text, so the global
 prefix is [0, n_txt + N_sh) (text, then the shared tokens in Hilbert order),
 and only the N_img - N_sh other image tokens, in Hilbert order, are tiled:
 the tile size N_T divides N_img - N_sh and the labels run over that span.
+
+A general shape (Appendix D: grid_h x grid_w, not a square power of two)
+takes the curve of its enclosing S x S grid (``hilbert.padded_perm``).  The
+image span then holds all S*S positions of that curve, in order; the
+positions whose cell lies outside the grid are padding.  Tiles, labels and
+the slide are taken over the S*S positions; the shared region is centred in
+the grid itself; padding is masked out as keys and as queries: a padding
+row attends nothing (its output is zero and its LSE -inf) and no row
+attends a padding key.  The moved layout is not defined for padded grids.
 """
 
 from dataclasses import dataclass
@@ -52,8 +61,24 @@ class Layout:
     moved: bool = False  # shared tokens gathered next to the text (Appendix A literally)
 
     @property
-    def n_img(self):
+    def side(self):
+        """Side S of the square the curve runs over (the grid itself when it
+        is a square power of two)."""
+        return hilbert.enclosing_side(self.grid_h, self.grid_w)
+
+    @property
+    def padded(self):
+        return self.side * self.side != self.grid_h * self.grid_w
+
+    @property
+    def n_cells(self):
+        """Image tokens of the grid."""
         return self.grid_h * self.grid_w
+
+    @property
+    def n_img(self):
+        """Positions of the image span: the S*S positions of the curve."""
+        return self.side * self.side
 
     @property
     def n_tot(self):
@@ -107,8 +132,21 @@ def shared_raster(layout):
 
 def shared_hilbert(layout):
     """Boolean over Hilbert positions p: True where token perm[p] is shared."""
-    perm, _ = hilbert.build_perm(layout.grid_h, layout.grid_w)
-    return shared_raster(layout)[perm]
+    perm, _ = hilbert.padded_perm(layout.grid_h, layout.grid_w)
+    out = np.zeros(perm.size, dtype=bool)
+    out[perm >= 0] = shared_raster(layout)[perm[perm >= 0]]
+    return out
+
+
+def valid_hilbert(layout):
+    """Boolean over Hilbert positions p: False at padding positions."""
+    perm, _ = hilbert.padded_perm(layout.grid_h, layout.grid_w)
+    return perm >= 0
+
+
+def token_valid(layout):
+    """Per sequence position: False at padding positions of the image span."""
+    return np.concatenate([np.ones(layout.n_txt, dtype=bool), valid_hilbert(layout)])
 
 
 def moved_perm(layout):
@@ -116,6 +154,8 @@ def moved_perm(layout):
     index of the token at image-span position d.  The shared tokens come
     first, in Hilbert order, then the other image tokens, in Hilbert order.
     """
+    if layout.padded:
+        raise ValueError("the moved layout needs a square power-of-two grid")
     hperm, _ = hilbert.build_perm(layout.grid_h, layout.grid_w)
     sh = shared_raster(layout)[hperm]
     return np.concatenate([hperm[sh], hperm[~sh]])
@@ -247,6 +287,9 @@ def mask_rows(layout, layer, rows):
     is_global, lab = token_classes(layout, layer)
     m = is_global[rows][:, None] | is_global[None, :]
     m |= (lab[rows][:, None] == lab[None, :]) & (lab[rows][:, None] >= 0)
+    if layout.padded:
+        ok = token_valid(layout)
+        m &= ok[rows][:, None] & ok[None, :]
     return m
 
 

@@ -9,24 +9,35 @@ order and perm[d] = raster index of Hilbert position d:
 
     permute:    y[b, d, :] = x[b, perm[d], :]
     unpermute:  x[b, perm[d], :] = y[b, d, :]
+
+A general shape (Appendix D) runs the curve over an enclosing grid; its
+padding slots carry perm[d] = -1.  The gather writes zero rows there (the
+values padding keys and queries carry, which the attention masks out) and
+the scatter leaves them out, so it restores exactly the grid's cells.
 """
 
 import numpy as np
 
 
 def permute(x, perm):
+    """y with one row per entry of perm (zero rows at padding slots)."""
     x = np.asarray(x)
     perm = np.asarray(perm, dtype=np.int64)
-    y = np.empty_like(x)
+    y = np.zeros((x.shape[0], perm.size) + x.shape[2:], dtype=x.dtype)
     for d in range(perm.size):
-        y[:, d, :] = x[:, perm[d], :]
+        if perm[d] >= 0:
+            y[:, d, :] = x[:, perm[d], :]
     return y
 
 
-def unpermute(y, perm):
+def unpermute(y, perm, n_out=None):
+    """x with n_out rows (default: one per entry of perm); padding slots of
+    y are dropped."""
     y = np.asarray(y)
     perm = np.asarray(perm, dtype=np.int64)
-    x = np.empty_like(y)
+    n_out = perm.size if n_out is None else n_out
+    x = np.zeros((y.shape[0], n_out) + y.shape[2:], dtype=y.dtype)
     for d in range(perm.size):
-        x[:, perm[d], :] = y[:, d, :]
+        if perm[d] >= 0:
+            x[:, perm[d], :] = y[:, d, :]
     return x

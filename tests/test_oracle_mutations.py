@@ -17,6 +17,7 @@ from oracle.schedule import Layout
 
 import test_oracle_accounting as t_acc
 import test_oracle_attention as t_att
+import test_oracle_general as t_gen
 import test_oracle_hilbert as t_hil
 import test_oracle_moved as t_mov
 import test_oracle_schedule as t_sch
@@ -50,6 +51,10 @@ PINS = [
     lambda: t_mov.test_tiles_partition_the_tiled_span(t_mov.MOVED[0], 1),
     lambda: t_mov.test_moved_sequence_equals_raster_construction(t_mov.MOVED[2], 1),
     lambda: t_mov.test_pattern_size_closed_form(t_mov.MOVED[3]),
+    lambda: t_gen.test_cells_follow_the_enclosing_turtle_curve(5, 7),
+    lambda: t_gen.test_shared_region_is_centred_in_the_grid(),
+    lambda: t_gen.test_padded_sequence_equals_raster_construction(t_gen.PADDED[1], 1),
+    lambda: t_gen.test_padding_content_does_not_reach_other_rows(t_gen.PADDED[0]),
 ]
 
 
@@ -116,7 +121,7 @@ def _mask_without_global_rows(orig):
 
 def _attention_with(mistake):
     """masked_attention with one planted mistake in its closed form."""
-    def f(q, k, v, mask_fn, scale=None, block=1024):
+    def f(q, k, v, mask_fn, scale=None, block=1024, empty_rows=False):
         q, k, v = (np.asarray(a, dtype=np.float64) for a in (q, k, v))
         b, h, n, d = q.shape
         scale = 1.0 / math.sqrt(d) if scale is None else scale
@@ -170,6 +175,25 @@ def _moved_parts_in_raster_order(orig):
     return f
 
 
+def _padding_keys_valid(orig):
+    return lambda layout: np.ones(layout.n_tot, dtype=bool)
+
+
+def _padded_grid_transposed(orig):
+    return lambda grid_h, grid_w: orig(grid_w, grid_h)
+
+
+def _region_centred_in_enclosing_grid(orig):
+    def f(layout):
+        side = layout.side
+        r0 = (side - layout.shared_h) // 2
+        c0 = (side - layout.shared_w) // 2
+        yy, xx = np.divmod(np.arange(layout.grid_h * layout.grid_w), layout.grid_w)
+        return ((yy >= r0) & (yy < r0 + layout.shared_h) & (xx >= c0) &
+                (xx < c0 + layout.shared_w))
+    return f
+
+
 MUTANTS = {
     "curve transposed": (hilbert, "xy_iterative", _xy_transposed),
     "curve without reflection": (hilbert, "xy_iterative", _xy_no_reflection),
@@ -187,6 +211,9 @@ MUTANTS = {
     "nnz drops the last row": (accounting, "nnz", _nnz_drops_last_block),
     "moved order is the plain curve": (schedule, "moved_perm", _moved_is_the_plain_curve),
     "moved parts in raster order": (schedule, "moved_perm", _moved_parts_in_raster_order),
+    "padding attended as keys and queries": (schedule, "token_valid", _padding_keys_valid),
+    "general grid transposed": (hilbert, "padded_perm", _padded_grid_transposed),
+    "region centred in the enclosing grid": (schedule, "shared_raster", _region_centred_in_enclosing_grid),
     "moved prefix without the shared tokens": (
         Layout, "prefix", lambda orig: property(lambda self: self.n_txt)),
 }
