@@ -278,6 +278,56 @@ def main():
     del s256
     torch.cuda.empty_cache()
 
+    # general shapes: the grid embedded in its enclosing power-of-two curve,
+    # padding masked; visited FLOPs count only pairs of real tokens, and the
+    # dense baseline runs over the unpadded sequence (text + grid cells)
+    def general_report(wname):
+        gw = synth.WORKLOADS[wname]
+        span = hb.image_span(gw.grid, gw.cols)
+        n_seq = gw.n_txt + span
+        cfg = hb.make_config(gw.grid, gw.n_txt, gw.tile, gw.delta, gw.shared, grid_w=gw.cols)
+        qg, kg, vg = (t.to(dev) for t in synth.qkv(gw.batch, gw.heads, n_seq, gw.head_dim, gw.dtype, seed=gw.seed))
+        og = torch.empty_like(qg)
+        sched = torch.empty(hb.hilberta_schedule_words(cfg), dtype=torch.int32, device=dev)
+        ws_b = hb.hilberta_attn_workspace_bytes(cfg, gw.batch, gw.heads, gw.head_dim, hb.HILBERTA_BF16)
+        wsg = torch.empty(max(ws_b, 16), dtype=torch.uint8, device=dev) if ws_b else None
+        pm = torch.empty(span, dtype=torch.int32, device=dev)
+        hb.hilberta_build_perm(gw.grid, gw.cols, pm)
+        valid = pm.cpu().numpy() >= 0
+        hb.hilberta_schedule(cfg, 0, sched)
+        tab = sched.cpu().numpy()
+        n_glob = gw.n_txt + gw.shared * gw.shared
+        nnz = n_glob * gw.n_tot
+        for qi in range(int(tab[4])):
+            start, len1, len2, ns = (int(x) for x in tab[12 + 4 * qi: 16 + 4 * qi])
+            p0 = start - gw.n_txt
+            nq = int(valid[p0:p0 + len1].sum() + valid[:len2].sum()) - ns
+            nnz += nq * (n_glob + nq)
+        call = lambda: hb.hilberta_attn_fwd(cfg, sched, qg, kg, vg, og, workspace=wsg)  # noqa: E731
+        call()
+        sp_ms = statistics.median(per_call(call, args.calls))
+        del qg, kg, vg, og
+        qd, kd, vd = (t.to(dev) for t in synth.qkv(gw.batch, gw.heads, gw.n_tot, gw.head_dim, gw.dtype, seed=gw.seed))
+        od = torch.empty_like(qd)
+        dws_b = hb.dense_attn_workspace_bytes(gw.batch, gw.heads, gw.n_tot, gw.head_dim, hb.HILBERTA_BF16)
+        dwsg = torch.empty(max(dws_b, 16), dtype=torch.uint8, device=dev) if dws_b else None
+        dcall = lambda: hb.dense_attn_fwd(qd, kd, vd, od, workspace=dwsg)  # noqa: E731
+        dcall()
+        de_ms = statistics.median(per_call(dcall, max(5, args.calls // 5)))
+        fl = 4 * gw.head_dim * gw.batch * gw.heads * nnz
+        return {
+            "shape": "%dx%d latent + %d text in the %dx%d curve, %d heads, D %d" % (
+                gw.grid, gw.cols, gw.n_txt, int(span ** 0.5), int(span ** 0.5), gw.heads, gw.head_dim),
+            "padding_fraction": round(1 - gw.n_img / span, 4),
+            "sparse_ms_per_call": round(sp_ms, 4),
+            "sparse_visited_tflops": round(fl / (sp_ms * 1e-3) / 1e12, 1),
+            "dense_unpadded_ms_per_call": round(de_ms, 4),
+            "speedup_vs_dense": round(de_ms / sp_ms, 2),
+        }
+
+    general = {name: general_report(name) for name in ("flux-96", "flux-64x96")}
+    torch.cuda.empty_cache()
+
     # ------------------------------------------------------- token gather
     # cold: a 512 MB write evicts the 256 MB last-level cache before each call
     flush = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device=dev)
@@ -363,6 +413,7 @@ def main():
         "sweep_64_57_layers": sweep,
         "paper_table1_settings": table1,
         "attn_256": rep256,
+        "general_shapes": general,
         "gather": gather,
         "wall_s_timed": round(wall, 3),
     }

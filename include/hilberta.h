@@ -21,10 +21,17 @@
  *            hilberta_last_error() returns a message for the calling thread's
  *            last failing call.  No C++ exception crosses this interface.
  * Sequence   The attention sequence of one (batch, head) is N_tot = n_txt +
- *            N_img tokens: text tokens at [0, n_txt), then the image tokens
- *            in Hilbert order at [n_txt, N_tot) (Appendix A places the text
- *            as a global prefix).  Shared-region tokens keep their Hilbert
- *            slots inside the image span.
+ *            N_img tokens: text tokens at [0, n_txt), then the image span in
+ *            Hilbert order at [n_txt, N_tot) (Appendix A places the text as
+ *            a global prefix).  Shared-region tokens keep their Hilbert
+ *            slots inside the image span (or follow the text, see layout).
+ * Shapes     A grid_h x grid_w grid that is not a square power of two takes
+ *            the curve of its enclosing S x S square, S the smallest power
+ *            of two >= max(grid_h, grid_w) and >= 2 (Appendix D).  The image
+ *            span then holds all N_img = S*S curve positions; the positions
+ *            whose cell lies outside the grid are padding slots, masked out
+ *            as keys and as queries.  For a square power-of-two grid,
+ *            S = grid_w and N_img = grid_h*grid_w.
  * Tensors    Q, K, V, O are [B, H, N_tot, D] with element strides given as
  *            {batch, head, row, dim}; the dim stride must be 1 and the other
  *            strides multiples of 8 elements (16-byte rows for bf16).
@@ -57,16 +64,18 @@ extern "C" {
 
 /*
  * Geometry of one HilbertA attention layer stack.
- *   grid_h, grid_w   latent grid; must be square with a power-of-two side in
- *                    [2, 32768] (the Hilbert curve of §3.1 lives on 2^k grids)
+ *   grid_h, grid_w   latent grid, each side in [1, 32768]; N_img = S*S
+ *                    image-span positions (see Shapes above)
  *   n_txt            text tokens placed before the image tokens (>= 0)
- *   tile             N_T, tokens per tile; divides grid_h*grid_w (§3.2)
+ *   tile             N_T, tokens per tile; divides N_img (§3.2)
  *   delta            per-layer advance Delta of the tile boundaries (>= 0);
  *                    the paper sets Delta = N_T / L for a slide cycle L (§3.2)
- *   shared_h/_w      central shared region (§3.3): image rows and columns in
- *                    [(side - s)/2, (side - s)/2 + s), integer halving; 0 x 0
- *                    disables it.  At most 1024 shared tokens (32 x 32,
- *                    the largest region the paper uses).
+ *   shared_h/_w      central shared region (§3.3): grid rows in
+ *                    [(grid_h - shared_h)/2, + shared_h) and columns in
+ *                    [(grid_w - shared_w)/2, + shared_w), integer halving;
+ *                    0 x 0 disables it.  At most 1024 shared tokens (32 x 32,
+ *                    the largest region the paper uses) and
+ *                    shared_h + shared_w <= 255.
  *   layout           HILBERTA_LAYOUT_IN_PLACE: the image span keeps all N_img
  *                    tokens in Hilbert order, the shared ones in their slots
  *                    (also global keys and dense rows), and is tiled whole.
@@ -76,7 +85,8 @@ extern "C" {
  *                    hilberta_build_perm_layout); the global prefix is the
  *                    text and the shared tokens, and only the N_img - N_sh
  *                    others are tiled, so `tile` must divide N_img - N_sh.
- * The sequence must satisfy n_txt + grid_h*grid_w < 2^31.
+ *                    Needs a square power-of-two grid (no padding).
+ * The sequence must satisfy n_txt + N_img < 2^31.
  */
 typedef struct hilberta_config {
     int32_t grid_h;
@@ -97,12 +107,13 @@ const char* hilberta_last_error(void);
 
 /*
  * hilberta_build_perm -- the Hilbert linearisation pi of §3.1.
- *   perm[d] = y*grid_w + x, where (x = column, y = row) is the cell at Hilbert
- *   position d, for d in [0, grid_h*grid_w).  The curve starts at (0, 0) and
- *   ends at (grid_w-1, 0).  If inv_or_null is not NULL, inv[perm[d]] = d.
- *   perm, inv: device int32 arrays of grid_h*grid_w entries.
- * Errors: EINVAL (perm NULL), EUNSUPPORTED (grid not square power of two in
- * [2, 32768]).
+ *   For each position d in [0, S*S) of the curve over the S x S square (S
+ *   as under Shapes; the curve starts at (0, 0) and ends at (S-1, 0)),
+ *   perm[d] = y*grid_w + x, where (x = column, y = row) is the cell at d,
+ *   or -1 when that cell lies outside the grid (a padding slot).  If
+ *   inv_or_null is not NULL, inv[y*grid_w + x] = d for every grid cell.
+ *   perm: device int32[S*S]; inv: device int32[grid_h*grid_w].
+ * Errors: EINVAL (perm NULL), EUNSUPPORTED (a side outside [1, 32768]).
  */
 int hilberta_build_perm(int32_t grid_h, int32_t grid_w, int32_t* perm,
                         int32_t* inv_or_null, void* stream);
@@ -112,8 +123,9 @@ int hilberta_build_perm(int32_t grid_h, int32_t grid_w, int32_t* perm,
  *   Hilbert linearisation (as hilberta_build_perm) in place; moved, the
  *   shared tokens first and then the others, each part in Hilbert order
  *   (Appendix A gathers the shared tokens next to the text).  perm[d] is the
- *   raster index of the token at image-span position d; if inv_or_null is
- *   not NULL, inv[perm[d]] = d.  perm, inv: device int32[grid_h*grid_w].
+ *   raster index of the token at image-span position d (-1 at padding
+ *   slots); if inv_or_null is not NULL, inv[perm[d]] = d for every grid
+ *   cell.  perm: device int32[N_img]; inv: device int32[grid_h*grid_w].
  * Errors: as hilberta_schedule_words for cfg; EINVAL (perm NULL).
  */
 int hilberta_build_perm_layout(const hilberta_config* cfg, int32_t* perm,
@@ -128,9 +140,13 @@ int hilberta_build_perm_layout(const hilberta_config* cfg, int32_t* perm,
  *             elements; strides in elements.  To leave text rows alone, pass
  *             pointers offset to the first image row.  x and y must not
  *             overlap.
- *   perm      device int32[n], a permutation of [0, n) (e.g. from
- *             hilberta_build_perm).  Entries outside [0, n) are not read
- *             through: such rows are skipped by the gather and the scatter.
+ *   perm      device int32[n] (e.g. from hilberta_build_perm): a
+ *             permutation of [0, n), or for a general shape an injection
+ *             into the grid's raster rows with -1 at padding slots.  A
+ *             negative entry makes the gather write a zero row y[b, d, :]
+ *             and the scatter skip x[b, d, :]; entries >= n are skipped by
+ *             both.  For a general shape, n = N_img rows of the sequence
+ *             side and the raster side has grid_h*grid_w rows.
  * Errors: EINVAL (NULL pointer, negative size, row stride < channels),
  * EUNSUPPORTED (dtype).
  */
@@ -190,6 +206,9 @@ int hilberta_attn_workspace_bytes(const hilberta_config* cfg, int64_t batch,
  *   rows of text and shared tokens attend all N_tot keys;
  *   every other image row attends the text keys, the shared keys and the
  *   keys of its own slid tile, each key once;
+ *   padding slots of a general shape are no key of any row, and their own
+ *   rows are written as O = 0 and lse = -inf.  Padding rows of K and V must
+ *   hold finite values (hilberta_permute writes zeros there);
  *   O = softmax(scale * Q K^T restricted to those keys) V, and optionally
  *   lse = ln sum exp(scale * q.k) over the same keys (natural log).
  *   sched      device table from hilberta_schedule(cfg, layer, ...); it

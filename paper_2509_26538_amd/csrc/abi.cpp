@@ -30,22 +30,38 @@ int hip_status(hipError_t e, const char* what) {
     return fail(HILBERTA_EHIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-bool pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
-
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+
+// Side of the square the curve runs over: the grid itself when it is a
+// square power of two, else the smallest enclosing power-of-two square, at
+// least 2 x 2 (Appendix D).  Sides must lie in [1, 32768].
+int32_t enclosing_side(int32_t grid_h, int32_t grid_w) {
+    const int32_t m = grid_h > grid_w ? grid_h : grid_w;
+    int32_t s = 2;
+    while (s < m) s *= 2;
+    return s;
+}
+
+int check_grid(int32_t grid_h, int32_t grid_w) {
+    if (grid_h < 1 || grid_w < 1 || grid_h > 32768 || grid_w > 32768)
+        return fail(HILBERTA_EUNSUPPORTED, "grid %dx%d: each side must lie in [1, 32768]", grid_h, grid_w);
+    return HILBERTA_OK;
+}
 
 int check_config(const hilberta_config* c) {
     if (!c) return fail(HILBERTA_EINVAL, "config is NULL");
     if (c->layout != HILBERTA_LAYOUT_IN_PLACE && c->layout != HILBERTA_LAYOUT_MOVED)
         return fail(HILBERTA_EINVAL, "layout %d is neither in place (0) nor moved (1)", c->layout);
-    if (c->grid_h != c->grid_w)
-        return fail(HILBERTA_EUNSUPPORTED, "grid %dx%d is not square", c->grid_h, c->grid_w);
-    if (!pow2(c->grid_w) || c->grid_w < 2 || c->grid_w > 32768)
-        return fail(HILBERTA_EUNSUPPORTED, "grid side %d is not a power of two in [2, 32768]",
-                    c->grid_w);
-    const int64_t n_img = (int64_t)c->grid_h * c->grid_w;
+    if (int rc = check_grid(c->grid_h, c->grid_w)) return rc;
+    const int32_t side = enclosing_side(c->grid_h, c->grid_w);
+    const bool padded = (int64_t)side * side != (int64_t)c->grid_h * c->grid_w;
+    if (padded && c->layout == HILBERTA_LAYOUT_MOVED)
+        return fail(HILBERTA_EUNSUPPORTED, "the moved layout needs a square power-of-two grid, not %dx%d",
+                    c->grid_h, c->grid_w);
+    // the image span: every position of the curve, padding included
+    const int64_t n_img = (int64_t)side * side;
     if (c->n_txt < 0) return fail(HILBERTA_EINVAL, "n_txt %d < 0", c->n_txt);
     if (c->n_txt + n_img > 0x7fffffffLL)
         return fail(HILBERTA_EUNSUPPORTED, "sequence of %lld tokens is too long",
@@ -81,8 +97,13 @@ struct Geom {
     int64_t prefix, tiled, shared_in_span, cap;
 };
 
+int64_t span_len(const hilberta_config* c) {
+    const int64_t side = enclosing_side(c->grid_h, c->grid_w);
+    return side * side;
+}
+
 Geom geom(const hilberta_config* c) {
-    const int64_t n_img = (int64_t)c->grid_h * c->grid_w;
+    const int64_t n_img = span_len(c);
     const int64_t n_sh = (int64_t)c->shared_h * c->shared_w;
     Geom g{};
     if (c->layout == HILBERTA_LAYOUT_MOVED) {
@@ -259,6 +280,12 @@ int run_attention(bool sparse, const hilberta_config* cfg, const int32_t* sched,
     a.total_items = (int32_t)p.total_items;
     a.n_bh = (int32_t)bh;
     a.sparse = sparse ? 1 : 0;
+    if (sparse && (int64_t)cfg->grid_h * cfg->grid_w != span_len(cfg)) {
+        a.padded = 1;
+        a.order = 31 - __builtin_clz((unsigned)enclosing_side(cfg->grid_h, cfg->grid_w));
+        a.grid_h = cfg->grid_h;
+        a.grid_w = cfg->grid_w;
+    }
     hipStream_t s = static_cast<hipStream_t>(stream);
     rc = hip_status(hilberta::launch_attn(a, dtype, (int)head_dim, s), "attention launch");
     if (rc || p.n_chunks == 1) return rc;
@@ -318,11 +345,9 @@ const char* hilberta_last_error(void) { return g_err.c_str(); }
 int hilberta_build_perm(int32_t grid_h, int32_t grid_w, int32_t* perm, int32_t* inv_or_null,
                         void* stream) {
     if (!perm) return fail(HILBERTA_EINVAL, "perm is NULL");
-    if (grid_h != grid_w || !pow2(grid_w) || grid_w < 2 || grid_w > 32768)
-        return fail(HILBERTA_EUNSUPPORTED, "grid %dx%d is not a square power of two in [2, 32768]",
-                    grid_h, grid_w);
-    return hip_status(hilberta::launch_build_perm(grid_w, perm, inv_or_null,
-                                                  static_cast<hipStream_t>(stream)),
+    if (int rc = check_grid(grid_h, grid_w)) return rc;
+    return hip_status(hilberta::launch_build_perm(enclosing_side(grid_h, grid_w), grid_h, grid_w, perm,
+                                                  inv_or_null, static_cast<hipStream_t>(stream)),
                       "build_perm launch");
 }
 
@@ -336,7 +361,9 @@ int hilberta_build_perm_layout(const hilberta_config* cfg, int32_t* perm, int32_
         return hip_status(hilberta::launch_build_perm_moved(cfg->grid_w, cfg->shared_h, cfg->shared_w, perm,
                                                             inv_or_null, s),
                           "build_perm launch");
-    return hip_status(hilberta::launch_build_perm(cfg->grid_w, perm, inv_or_null, s), "build_perm launch");
+    return hip_status(hilberta::launch_build_perm(enclosing_side(cfg->grid_h, cfg->grid_w), cfg->grid_h,
+                                                  cfg->grid_w, perm, inv_or_null, s),
+                      "build_perm launch");
 }
 
 int hilberta_permute(const void* x, void* y, const int32_t* perm, int64_t batch, int64_t n,
@@ -377,6 +404,7 @@ int hilberta_schedule(const hilberta_config* cfg, int32_t layer, int32_t* sched,
     a.out = sched;
     a.grid_h = cfg->grid_h;
     a.grid_w = cfg->grid_w;
+    a.side = enclosing_side(cfg->grid_h, cfg->grid_w);
     a.n_txt = cfg->n_txt;
     a.tile = cfg->tile;
     a.n_tiles = (int32_t)(g.tiled / cfg->tile);
@@ -402,7 +430,7 @@ int hilberta_attn_workspace_bytes(const hilberta_config* cfg, int64_t batch, int
         return fail(HILBERTA_EUNSUPPORTED, "head_dim %lld not in {64, 128}", (long long)head_dim);
     if (dtype != HILBERTA_F32 && dtype != HILBERTA_BF16) return fail(HILBERTA_EUNSUPPORTED, "dtype %d", dtype);
     const Geom g = geom(cfg);
-    const int64_t n_tot = cfg->n_txt + (int64_t)cfg->grid_h * cfg->grid_w;
+    const int64_t n_tot = cfg->n_txt + span_len(cfg);
     const Plan p = make_plan(true, g.prefix, g.tiled, g.shared_in_span, cfg->tile, n_tot, batch * heads,
                              head_dim, dtype, true);
     *bytes = p.ws_bytes;
@@ -417,7 +445,7 @@ int hilberta_attn_fwd(const hilberta_config* cfg, const int32_t* sched, const vo
     int rc = check_config(cfg);
     if (rc) return rc;
     if (!sched) return fail(HILBERTA_EINVAL, "sched is NULL");
-    const int64_t n_tot = cfg->n_txt + (int64_t)cfg->grid_h * cfg->grid_w;
+    const int64_t n_tot = cfg->n_txt + span_len(cfg);
     return run_attention(true, cfg, sched, q, k, v, o, lse_or_null, batch, heads, n_tot, head_dim,
                          q_strides, k_strides, v_strides, o_strides, dtype, scale, workspace,
                          workspace_bytes, stream);

@@ -111,6 +111,7 @@ __global__ void __launch_bounds__(kThreads, 1) attn_f32_kernel(AttnArgs a) {
     const int32_t chunk = dense ? r % a.n_chunks : 0;
     const int32_t row0 = dense ? (r / a.n_chunks) * kBlockM : (r - dense_items) * kBlockM;
     const Segs g = item_segments<kBN>(a, dense, chunk, row0, kBlockM, n_shared, mc);
+    const int32_t lm = mc.label_mask | (a.padded ? 2 : 0);
     const RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockM, mc.o, n_shared, sm.sp);
 
     const int32_t bb = bh / a.heads;
@@ -135,15 +136,15 @@ __global__ void __launch_bounds__(kThreads, 1) attn_f32_kernel(AttnArgs a) {
     LoaderF32<D> ld;
     ld.init(kb, vb, a);
     const int nblk = g.e3;
-    ld.load(BLOCK_AT(kBN, 0, g, mc.label_mask), mc, a, sm.sp, tid, n_shared);
+    ld.load(BLOCK_AT(kBN, 0, g, lm), mc, a, sm.sp, tid, n_shared);
     ld.store(sm.st, 0, tid);
-    if (nblk > 1) ld.load(BLOCK_AT(kBN, 1, g, mc.label_mask), mc, a, sm.sp, tid, n_shared);
+    if (nblk > 1) ld.load(BLOCK_AT(kBN, 1, g, lm), mc, a, sm.sp, tid, n_shared);
     __syncthreads();
     for (int i = 0; i < nblk; ++i) {
         const int buf = i & 1;
         if (i + 1 < nblk) ld.store(sm.st, buf ^ 1, tid);
-        if (i + 2 < nblk) ld.load(BLOCK_AT(kBN, i + 2, g, mc.label_mask), mc, a, sm.sp, tid, n_shared);
-        const Block b = BLOCK_AT(kBN, i, g, mc.label_mask);
+        if (i + 2 < nblk) ld.load(BLOCK_AT(kBN, i + 2, g, lm), mc, a, sm.sp, tid, n_shared);
+        const Block b = BLOCK_AT(kBN, i, g, lm);
         // S^T: s[kt] holds keys 32 kt + 8 (e/4) + 4 h + e%4 against this row
         f32x16 s[2];
 #pragma unroll

@@ -40,6 +40,12 @@
 // The running sum is kept in fp32 as four independent partial sums.  The
 // reference max moves only when a row max grows by more than 2^8 (acc and l
 // share it, so it cancels in acc / l).
+//
+// General shapes: when the image span holds padding positions, wavefront 0
+// classifies every key of a stage while it is loaded (the curve position
+// decoded to its cell) and flags the stage for the per-key masks only if a
+// key is padding or needs a label; a query block made of padding rows only
+// stores its empty-softmax rows without visiting any key.
 #include "attn_common.hpp"
 
 namespace hilberta {
@@ -66,6 +72,7 @@ struct Smem {
     alignas(16) int32_t info[2][kBN];
     Spans sp;
     int32_t n_keep;
+    int32_t slow[2];  // padded spans: stage needs the per-key masks
 };
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -182,6 +189,15 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
 
     const int32_t bb = bh / a.heads;
     const int32_t hh = bh - bb * a.heads;
+    if (a.padded && !dense && !__syncthreads_or(ri.store && !ri.pad)) {
+        // nothing but padding rows (and rows stored elsewhere): no keys
+        f32x16 zero[D / 32];
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) zero[dt] = f32x16{};
+        __bf16* ob = reinterpret_cast<__bf16*>(a.o) + bb * a.o_sb + hh * a.o_sh;
+        store_row<__bf16, D>(a, ri, bh, chunk, dense, h, -INFINITY, 0.f, zero, ob);
+        return;
+    }
     const __bf16* qrow = reinterpret_cast<const __bf16*>(a.q) + bb * a.q_sb + hh * a.q_sh + (int64_t)ri.qseq * a.q_sr;
     const __bf16* kbase = reinterpret_cast<const __bf16*>(a.k) + bb * a.k_sb + hh * a.k_sh;
     const __bf16* vbase = reinterpret_cast<const __bf16*>(a.v) + bb * a.v_sb + hh * a.v_sh;
@@ -242,7 +258,23 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
                 dma16(vrs, vl + j * 1024, key * vrow_b + vcol[j]);
             }
         }
-        if (!stage_fast(i) && tid < kBN) {
+        if (a.padded) {
+            if (tid < kBN) {
+                const int32_t v = v0 + tid;
+                int32_t inf = kKeyInvalid;
+                if (v < total) {
+                    const int32_t seq = base >= 0 ? base + tid : list_seq(v, b1, b2, b3, s0, sa, sb, sm.sp);
+                    if (!seq_padding(a, seq)) {
+                        inf = kKeyAll;
+                        if (label_mask && v >= b2 && !is_shared_seq(sm.sp, seq))
+                            inf = tile_label(seq - a.n_txt, o, a.tile, a.n_img);
+                    }
+                }
+                sm.info[buf][tid] = inf;
+                const bool slow = __builtin_amdgcn_ballot_w64(inf != kKeyAll) != 0;
+                if (tid == 0) sm.slow[buf] = slow;
+            }
+        } else if (!stage_fast(i) && tid < kBN) {
             const int32_t v = v0 + tid;
             int32_t inf = kKeyInvalid;
             if (v < total) {
@@ -316,7 +348,7 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
                 vop[cc][dt] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
             }
         __builtin_amdgcn_sched_barrier(0);
-        if (!stage_fast(i)) {
+        if (a.padded ? sm.slow[buf] != 0 : !stage_fast(i)) {
 #pragma unroll
             for (int kt = 0; kt < 2; ++kt)
 #pragma unroll

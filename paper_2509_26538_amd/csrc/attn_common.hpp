@@ -17,8 +17,15 @@
 // masked in the shared segment (fp32 kernel) or left out of it (bf16
 // kernel).  Rows of shared tokens inside a sparse item are computed by the
 // dense items and not stored by the sparse item.
+//
+// General shapes (Appendix D): the image span holds every position of the
+// enclosing square's curve; a position whose cell lies outside the grid is
+// padding.  Padding keys are masked for every row (stages that hold one take
+// the per-key mask path), and padding rows are stored as an empty softmax:
+// O = 0, LSE = -inf.
 #pragma once
 
+#include "curve.hpp"
 #include "internal.hpp"
 
 namespace hilberta {
@@ -107,6 +114,18 @@ __device__ __forceinline__ int32_t tile_label(int32_t p, int32_t o, int32_t tile
     return ((p + o) % n_img) / tile;
 }
 
+// Is image position p (0 <= p < n_img) a cell of the grid, not padding?
+__device__ __forceinline__ bool pos_valid(const AttnArgs& a, int32_t p) {
+    uint32_t x, y;
+    hilbert_d2xy(a.order, (uint32_t)p, x, y);
+    return x < (uint32_t)a.grid_w && y < (uint32_t)a.grid_h;
+}
+
+// Is sequence position seq a padding slot?
+__device__ __forceinline__ bool seq_padding(const AttnArgs& a, int32_t seq) {
+    return a.padded && seq >= a.n_txt && !pos_valid(a, seq - a.n_txt);
+}
+
 template <int BN>
 __device__ __forceinline__ Block block_at(int32_t i, int32_t b0, int32_t b1, int32_t b2, int32_t b3,
                                           int32_t l0, int32_t l1, int32_t l2, int32_t l3,
@@ -122,7 +141,9 @@ __device__ __forceinline__ Block block_at(int32_t i, int32_t b0, int32_t b1, int
     b.first = (i - before) * BN;
     b.base = base + b.first;
     b.cnt = min(BN, len - b.first);
-    b.fast = b.cnt == BN && (kind == SEG_CONTIG || (kind == SEG_TILE && !label_mask));
+    // label_mask bit 0: per-row tile labels; bit 1: the image span has
+    // padding, so every stage takes the per-key masks
+    b.fast = b.cnt == BN && !(label_mask & 2) && (kind == SEG_CONTIG || (kind == SEG_TILE && !(label_mask & 1)));
     return b;
 }
 
@@ -158,6 +179,7 @@ __device__ __forceinline__ int32_t key_seq(const Block& b, int32_t r, const Span
 __device__ __forceinline__ int32_t key_info(const Block& b, int32_t r, int32_t seq, MaskCtx it,
                                             const AttnArgs& a, const Spans& sp) {
     if (r >= b.cnt) return kKeyInvalid;
+    if (b.kind != SEG_SHARED && seq_padding(a, seq)) return kKeyInvalid;
     if (b.kind == SEG_CONTIG) return kKeyAll;
     const int32_t p = seq - a.n_txt;
     if (b.kind == SEG_SHARED) {
@@ -242,12 +264,13 @@ struct RowInfo {
     int32_t dense_row;
     int32_t label;
     bool store;
+    bool pad;  // a padding row: stored as O = 0, LSE = -inf
 };
 
 __device__ __forceinline__ RowInfo row_info(const AttnArgs& a, bool dense, int32_t row0,
                                             int32_t rr, int32_t block_m, int32_t o,
                                             int32_t n_shared, const Spans& sp) {
-    RowInfo ri{0, -1, -3, false};
+    RowInfo ri{0, -1, -3, false, false};
     if (dense) {
         ri.dense_row = row0 + rr;
         if (ri.dense_row < a.n_dense_rows) {
@@ -267,6 +290,7 @@ __device__ __forceinline__ RowInfo row_info(const AttnArgs& a, bool dense, int32
         ri.qseq = a.n_txt + pc;
         ri.store = ok && !is_shared_seq(sp, ri.qseq);
         ri.label = tile_label(pc, o, a.tile, a.n_img);
+        ri.pad = ok && seq_padding(a, ri.qseq);
     }
     return ri;
 }
@@ -329,6 +353,14 @@ __device__ __forceinline__ void store_row(const AttnArgs& a, const RowInfo& ri, 
     if (!ri.store) return;
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
     T* orow = obase + (int64_t)ri.qseq * a.o_sr;
+    if (ri.pad) {
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) store4<T>(orow + 32 * dt + 8 * g + 4 * h, 0.f, 0.f, 0.f, 0.f);
+        if (a.lse && h == 0) a.lse[(int64_t)bh * a.n_tot + ri.qseq] = -INFINITY;
+        return;
+    }
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll

@@ -1,73 +1,31 @@
 // Hilbert linearisation (§3.1) and the per-layer schedule table (§3.2, §3.3).
 //
-// The Hilbert position d of a cell is decoded digit by digit: the base-4
-// digits of d, from the least significant, say which quadrant of the next
-// larger square the partial curve lies in and whether it is transposed
-// (and reflected) there.  Orientation: start (0, 0), end (side-1, 0),
-// x = column, y = row, raster index y*side + x.
+// A grid of grid_h x grid_w cells takes the curve of its enclosing square of
+// side S = 2^order (the grid itself when it is a square power of two; the
+// smallest enclosing power-of-two square otherwise, Appendix D).  Curve
+// position d decodes to the cell (x, y), x = column, y = row; the cell is
+// the grid's raster index y*grid_w + x when x < grid_w and y < grid_h, and a
+// padding slot otherwise.
+#include "curve.hpp"
 #include "internal.hpp"
 
 namespace hilberta {
 namespace {
 
-__device__ inline void hilbert_d2xy(int order, uint32_t d, uint32_t& x, uint32_t& y) {
-    uint32_t px = 0, py = 0;
-    for (int lvl = 0; lvl < order; ++lvl) {
-        const uint32_t s = 1u << lvl;
-        const uint32_t digit = (d >> (2 * lvl)) & 3u;
-        const uint32_t rx = digit >> 1;
-        const uint32_t ry = (digit ^ rx) & 1u;
-        if (ry == 0) {
-            if (rx) {
-                px = s - 1 - px;
-                py = s - 1 - py;
-            }
-            const uint32_t t = px;
-            px = py;
-            py = t;
-        }
-        px += s * rx;
-        py += s * ry;
-    }
-    x = px;
-    y = py;
-}
 
-// Inverse of hilbert_d2xy: peel the most significant quadrant first.
-__device__ inline uint32_t hilbert_xy2d(int order, uint32_t x, uint32_t y) {
-    uint32_t d = 0;
-    for (int lvl = order - 1; lvl >= 0; --lvl) {
-        const uint32_t s = 1u << lvl;
-        const uint32_t rx = (x >> lvl) & 1u;
-        const uint32_t ry = (y >> lvl) & 1u;
-        d += s * s * ((3u * rx) ^ ry);
-        x &= s - 1;
-        y &= s - 1;
-        if (ry == 0) {
-            const uint32_t t = x;
-            x = y;
-            y = t;
-            if (rx) {
-                x = s - 1 - x;
-                y = s - 1 - y;
-            }
-        }
-    }
-    return d;
-}
 
-__device__ inline int log2_side(int32_t side) { return 31 - __clz(side); }
-
-__global__ void __launch_bounds__(256) build_perm_kernel(int32_t side, int32_t* __restrict__ perm,
+__global__ void __launch_bounds__(256) build_perm_kernel(int32_t side, int32_t grid_h, int32_t grid_w,
+                                                         int32_t* __restrict__ perm,
                                                          int32_t* __restrict__ inv) {
     const int order = log2_side(side);
     const uint32_t n = (uint32_t)side * (uint32_t)side;
     for (uint32_t d = blockIdx.x * blockDim.x + threadIdx.x; d < n; d += gridDim.x * blockDim.x) {
         uint32_t x, y;
         hilbert_d2xy(order, d, x, y);
-        const uint32_t raster = y * (uint32_t)side + x;
-        perm[d] = (int32_t)raster;
-        if (inv) inv[raster] = (int32_t)d;
+        const bool cell = x < (uint32_t)grid_w && y < (uint32_t)grid_h;
+        const uint32_t raster = y * (uint32_t)grid_w + x;
+        perm[d] = cell ? (int32_t)raster : -1;
+        if (inv && cell) inv[raster] = (int32_t)d;
     }
 }
 
@@ -84,13 +42,15 @@ struct RunsLds {
     int32_t n_starts, n_ends;
 };
 
-__device__ int32_t shared_runs(RunsLds& r, int32_t side, int32_t shared_h, int32_t shared_w,
-                               int32_t cap) {
+__device__ int32_t shared_runs(RunsLds& r, int32_t side, int32_t grid_h, int32_t grid_w, int32_t shared_h,
+                               int32_t shared_w, int32_t cap) {
     const int tid = threadIdx.x;
     const int order = log2_side(side);
     const uint32_t n_img = (uint32_t)side * (uint32_t)side;
-    const int32_t r0 = (side - shared_h) / 2;
-    const int32_t c0 = (side - shared_w) / 2;
+    // the region is centred in the grid (which sits at the origin of the
+    // enclosing square), so none of its cells is padding
+    const int32_t r0 = (grid_h - shared_h) / 2;
+    const int32_t c0 = (grid_w - shared_w) / 2;
     const int32_t n_cells = shared_h * shared_w;
     if (tid == 0) {
         r.n_starts = 0;
@@ -138,7 +98,7 @@ __global__ void __launch_bounds__(256) shared_runs_kernel(ScheduleArgs a) {
     __shared__ RunsLds r;
     const int tid = threadIdx.x;
     const int32_t n_cells = a.shared_h * a.shared_w;
-    const int32_t n_runs = a.moved || n_cells == 0 ? 0 : shared_runs(r, a.grid_w, a.shared_h, a.shared_w, a.span_cap);
+    const int32_t n_runs = a.moved || n_cells == 0 ? 0 : shared_runs(r, a.side, a.grid_h, a.grid_w, a.shared_h, a.shared_w, a.span_cap);
     int32_t* spans = a.out + 12 + 4 * a.n_tiles;
     for (int32_t i = tid; i < n_runs; i += blockDim.x) {
         spans[2 * i] = a.prefix + r.sorted_starts[i];
@@ -174,7 +134,7 @@ __global__ void __launch_bounds__(256) build_perm_moved_kernel(int32_t side, int
                                                                int32_t* __restrict__ perm,
                                                                int32_t* __restrict__ inv) {
     __shared__ RunsLds r;
-    const int32_t n_runs = shared_runs(r, side, shared_h, shared_w, kMaxSpans);
+    const int32_t n_runs = shared_runs(r, side, side, side, shared_h, shared_w, kMaxSpans);
     const int order = log2_side(side);
     const uint32_t n = (uint32_t)side * (uint32_t)side;
     const int32_t n_sh = shared_h * shared_w;
@@ -224,11 +184,12 @@ __global__ void __launch_bounds__(256) tiles_kernel(ScheduleArgs a) {
 
 }  // namespace
 
-hipError_t launch_build_perm(int32_t side, int32_t* perm, int32_t* inv, hipStream_t s) {
+hipError_t launch_build_perm(int32_t side, int32_t grid_h, int32_t grid_w, int32_t* perm, int32_t* inv,
+                             hipStream_t s) {
     const int64_t n = (int64_t)side * side;
     const int64_t want = (n + 255) / 256;
     const int blocks = (int)(want < 65536 ? want : 65536);
-    hipLaunchKernelGGL(build_perm_kernel, dim3(blocks), dim3(256), 0, s, side, perm, inv);
+    hipLaunchKernelGGL(build_perm_kernel, dim3(blocks), dim3(256), 0, s, side, grid_h, grid_w, perm, inv);
     return hipGetLastError();
 }
 

@@ -52,6 +52,12 @@ struct AttnArgs {
     int32_t total_items;
     int32_t n_bh;        // batch * heads
     int32_t sparse;      // 1: HilbertA pattern, 0: dense baseline
+    // general shapes: the image span holds the 2^order x 2^order curve
+    // positions of the enclosing square, those whose cell lies outside the
+    // grid_h x grid_w grid being padding (masked as keys and queries)
+    int32_t padded;      // 1 when some image positions are padding
+    int32_t order;
+    int32_t grid_h, grid_w;
 };
 
 struct MergeArgs {
@@ -77,13 +83,17 @@ hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& m, int dtype, int head_dim, hipStream_t s);
 
 // ----------------------------------------------------- permutation, schedule
-hipError_t launch_build_perm(int32_t side, int32_t* perm, int32_t* inv, hipStream_t s);
+// perm[d] for the side x side curve positions: the raster index of the
+// grid_h x grid_w grid's cell at d, or -1 for a padding slot
+hipError_t launch_build_perm(int32_t side, int32_t grid_h, int32_t grid_w, int32_t* perm, int32_t* inv,
+                             hipStream_t s);
 hipError_t launch_build_perm_moved(int32_t side, int32_t shared_h, int32_t shared_w, int32_t* perm,
                                    int32_t* inv, hipStream_t s);
 
 struct ScheduleArgs {
     int32_t* out;
     int32_t grid_h, grid_w, n_txt, tile, n_tiles, shared_h, shared_w;
+    int32_t side;       // side of the square the curve runs over
     int32_t prefix;     // global prefix: n_txt, plus the shared tokens when moved
     int32_t tiled;      // tokens of the tiled span: N_img, or N_img - N_sh when moved
     int32_t moved;      // 1: shared tokens gathered next to the text

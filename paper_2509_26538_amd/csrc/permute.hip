@@ -1,6 +1,9 @@
 // Token gather / scatter along the Hilbert order (§3.4):
 //   gather   y[b, d, :] = x[b, perm[d], :]
 //   scatter  y[b, perm[d], :] = x[b, d, :]
+// perm[d] < 0 marks a padding slot of a general shape (Appendix D): the
+// gather writes a zero row there and the scatter skips it.  Entries >= n
+// are skipped by both.
 // Rows are copied as raw bytes.  The copy is HBM-bound and touches every
 // byte once, so the row kernel's loads and stores are non-temporal: streamed
 // through without displacing cached data, which on a cold copy is worth over
@@ -48,6 +51,9 @@ __global__ void __launch_bounds__(kCopyThreads) permute_kernel(PermuteArgs a, I 
                 const char* src = a.x + b * a.x_bs + src_row * a.x_rs + col * (int64_t)sizeof(V);
                 buf[u] = *reinterpret_cast<const V*>(src);
                 dst[u] = b * a.y_bs + dst_row * a.y_rs + col * (int64_t)sizeof(V);
+            } else if (p < 0 && !a.scatter) {
+                buf[u] = V{};
+                dst[u] = b * a.y_bs + d * a.y_rs + col * (int64_t)sizeof(V);
             }
         }
     }
@@ -72,11 +78,16 @@ __global__ void __launch_bounds__(kCopyThreads) permute_rows_kernel(PermuteArgs 
         const int64_t b = row / a.n;
         const int64_t d = row - b * a.n;
         const int32_t p = a.perm[d];
-        if (p < 0 || p >= a.n) continue;
-        const int64_t src_row = a.scatter ? d : p;
+        if (p >= a.n || (p < 0 && a.scatter)) continue;
         const int64_t dst_row = a.scatter ? p : d;
-        const V* src = reinterpret_cast<const V*>(a.x + b * a.x_bs + src_row * a.x_rs);
         V* dst = reinterpret_cast<V*>(a.y + b * a.y_bs + dst_row * a.y_rs);
+        if (p < 0) {
+            // padding slot: a zero row
+            for (int32_t c = lane; c < vec_per_row; c += 64) __builtin_nontemporal_store(V{}, dst + c);
+            continue;
+        }
+        const int64_t src_row = a.scatter ? d : p;
+        const V* src = reinterpret_cast<const V*>(a.x + b * a.x_bs + src_row * a.x_rs);
         for (int32_t c0 = 0; c0 < vec_per_row; c0 += 64 * U) {
             V buf[U];
 #pragma unroll

@@ -124,11 +124,23 @@ def _dtype(t):
     raise HilbertaError(HILBERTA_EUNSUPPORTED, "dtype %s" % t.dtype)
 
 
-def make_config(grid, n_txt, tile, delta, shared_h=0, shared_w=None, layout=LAYOUT_IN_PLACE):
-    """hilberta_config for a grid x grid latent grid."""
+def make_config(grid, n_txt, tile, delta, shared_h=0, shared_w=None, layout=LAYOUT_IN_PLACE,
+                grid_w=None):
+    """hilberta_config for a grid x grid_w latent grid (square by default)."""
     if shared_w is None:
         shared_w = shared_h
-    return hilberta_config(grid, grid, n_txt, tile, delta, shared_h, shared_w, layout)
+    return hilberta_config(grid, grid if grid_w is None else grid_w, n_txt, tile, delta, shared_h,
+                           shared_w, layout)
+
+
+def image_span(grid_h, grid_w):
+    """N_img, the image-span length of a grid_h x grid_w grid as the header
+    defines it: S*S with S the smallest power of two >= max(grid_h, grid_w)
+    and >= 2 (perm buffers and sequences are sized by it)."""
+    side = 2
+    while side < max(grid_h, grid_w):
+        side *= 2
+    return side * side
 
 
 def hilberta_version():
@@ -145,25 +157,34 @@ def hilberta_build_perm_layout(cfg, perm, inv=None, stream=None):
 
 
 def _permute(name, x, y, perm, stream):
-    if x.dim() != 3 or y.dim() != 3 or x.shape != y.shape:
-        raise HilbertaError(HILBERTA_EINVAL, "x and y must be [B, N, C] of one shape")
+    # the sequence side (y of the gather, x of the scatter) has one row per
+    # perm entry; the raster side may have fewer rows (padding slots of a
+    # general shape, perm entry -1)
+    if x.dim() != 3 or y.dim() != 3 or x.shape[0] != y.shape[0] or x.shape[2] != y.shape[2]:
+        raise HilbertaError(HILBERTA_EINVAL, "x and y must be [B, N, C] with one B and C")
     if x.stride(2) != 1 or y.stride(2) != 1:
         raise HilbertaError(HILBERTA_EUNSUPPORTED, "channels must be contiguous")
     if x.dtype != y.dtype:
         raise HilbertaError(HILBERTA_EINVAL, "x and y dtypes differ")
-    b, n, c = x.shape
+    seq, raster = (y, x) if name == "hilberta_permute" else (x, y)
+    if perm.numel() != seq.shape[1] or raster.shape[1] > seq.shape[1]:
+        raise HilbertaError(HILBERTA_EINVAL, "perm must have one entry per sequence row, and the "
+                                             "raster side no more rows than the sequence side")
+    b, n, c = seq.shape
     fn = getattr(load(), name)
     _check(fn(_ptr(x), _ptr(y), _ptr(perm), b, n, c, x.stride(0), x.stride(1),
               y.stride(0), y.stride(1), _dtype(x), _stream(stream)))
 
 
 def hilberta_permute(x, y, perm, stream=None):
-    """y[b, d, :] = x[b, perm[d], :] for x, y of shape [B, N, C]."""
+    """y[b, d, :] = x[b, perm[d], :] (a zero row where perm[d] < 0) for
+    y [B, N, C] with N = perm entries and x [B, N', C], N' <= N."""
     _permute("hilberta_permute", x, y, perm, stream)
 
 
 def hilberta_unpermute(x, y, perm, stream=None):
-    """y[b, perm[d], :] = x[b, d, :] for x, y of shape [B, N, C]."""
+    """y[b, perm[d], :] = x[b, d, :] (skipped where perm[d] < 0) for
+    x [B, N, C] with N = perm entries and y [B, N', C], N' <= N."""
     _permute("hilberta_unpermute", x, y, perm, stream)
 
 

@@ -32,13 +32,22 @@ class Workload:
     hidden: int = 3072    # hidden size of the token gather workload
     seed: int = 0
     moved: bool = False   # shared tokens gathered next to the text (Appendix A)
+    grid_w: int = 0       # grid columns when the grid is not square (0: square)
+
+    @property
+    def cols(self):
+        return self.grid_w or self.grid
 
     @property
     def n_img(self):
-        return self.grid * self.grid
+        """Image tokens of the grid (grid x cols cells)."""
+        return self.grid * self.cols
 
     @property
     def n_tot(self):
+        """Text plus image tokens.  A grid that is not a square power of two
+        runs attention over a longer, padded sequence (see image_span in the
+        binding)."""
         return self.n_txt + self.n_img
 
 
@@ -64,6 +73,11 @@ WORKLOADS = {
     "table1-128-g16": Workload("table1-128-g16", 128, 512, 1, 24, 128, "bf16", 1024, 256, 32),
     # the same settings in the moved-prefix layout of Appendix A: the shared
     # tokens follow the text and the other N_img - N_sh tokens form G tiles
+    # general shapes (Appendix D): Flux.1-dev at 1536x1536 (96x96 latent) and
+    # at 1024x1536 portrait (64 rows x 96 columns), both in the 128x128
+    # enclosing curve
+    "flux-96": Workload("flux-96", 96, 512, 1, 24, 128, "bf16", 1024, 512, 16),
+    "flux-64x96": Workload("flux-64x96", 64, 512, 1, 24, 128, "bf16", 1024, 512, 16, grid_w=96),
     "moved-64-g4": Workload("moved-64-g4", 64, 512, 1, 24, 128, "bf16", 960, 240, 16, moved=True),
     "moved-64-g16": Workload("moved-64-g16", 64, 512, 1, 24, 128, "bf16", 240, 60, 16, moved=True),
     "moved-128-g4": Workload("moved-128-g4", 128, 512, 1, 24, 128, "bf16", 3840, 960, 32, moved=True),

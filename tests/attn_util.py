@@ -23,7 +23,7 @@ def config_of(layout):
 
 
 def layout_of(w):
-    return Layout(w.grid, w.grid, w.n_txt, w.tile, w.delta, w.shared, w.shared, moved=w.moved)
+    return Layout(w.grid, w.cols, w.n_txt, w.tile, w.delta, w.shared, w.shared, moved=w.moved)
 
 
 def make_schedule(layout, layer, dev):
@@ -71,7 +71,8 @@ def hip_dense(q, k, v, dev, split=True):
 
 def oracle_sparse(layout, layer, q, k, v):
     q64, k64, v64 = (t.to(torch.float64).numpy() for t in (q, k, v))
-    return attention.masked_attention(q64, k64, v64, lambda rows: schedule.mask_rows(layout, layer, rows))
+    return attention.masked_attention(q64, k64, v64, lambda rows: schedule.mask_rows(layout, layer, rows),
+                                      empty_rows=layout.padded)
 
 
 def oracle_rows(layout, layer, q, k, v, rows):
@@ -79,6 +80,15 @@ def oracle_rows(layout, layer, q, k, v, rows):
     m = schedule.mask_rows(layout, layer, rows) if layout is not None else np.ones(
         (len(rows), q.shape[2]), dtype=bool)
     return attention.masked_attention_rows(q64, k64, v64, rows, m)
+
+
+def assert_lse_close(got, ref, tol):
+    """LSE within tol where finite; -inf (empty rows) exactly where the
+    reference has it."""
+    empty = np.isneginf(ref)
+    assert np.array_equal(np.isneginf(got), empty), "empty-row LSE pattern differs"
+    if (~empty).any():
+        assert np.abs(got[~empty] - ref[~empty]).max() <= tol
 
 
 def assert_close(got, ref, dtype, what="", max_abs=None):

@@ -42,8 +42,9 @@ def code(fn, *args):
     return rc
 
 
-@pytest.mark.parametrize("h,w,rc", [(3, 3, hb.HILBERTA_EUNSUPPORTED), (4, 8, hb.HILBERTA_EUNSUPPORTED),
-                                    (1, 1, hb.HILBERTA_EUNSUPPORTED), (65536, 65536, hb.HILBERTA_EUNSUPPORTED)])
+@pytest.mark.parametrize("h,w,rc", [(0, 4, hb.HILBERTA_EUNSUPPORTED), (4, 0, hb.HILBERTA_EUNSUPPORTED),
+                                    (-3, 3, hb.HILBERTA_EUNSUPPORTED), (40000, 2, hb.HILBERTA_EUNSUPPORTED),
+                                    (65536, 65536, hb.HILBERTA_EUNSUPPORTED)])
 def test_build_perm_rejects_bad_grids(lib, h, w, rc):
     assert lib.hilberta_build_perm(h, w, FAKE, None, None) == rc
     assert "grid" in hb.last_error()
@@ -54,8 +55,10 @@ def test_build_perm_rejects_null(lib):
 
 
 BAD_CONFIGS = [
-    (hb.hilberta_config(8, 16, 0, 16, 4, 0, 0), hb.HILBERTA_EUNSUPPORTED),   # not square
-    (hb.hilberta_config(6, 6, 0, 4, 2, 0, 0), hb.HILBERTA_EUNSUPPORTED),     # not 2^k
+    (hb.hilberta_config(0, 16, 0, 16, 4, 0, 0), hb.HILBERTA_EUNSUPPORTED),   # empty grid
+    (hb.hilberta_config(6, 6, 0, 7, 2, 0, 0), hb.HILBERTA_EUNSUPPORTED),     # tile does not divide 8x8
+    (hb.hilberta_config(6, 6, 0, 4, 2, 0, 0, 1), hb.HILBERTA_EUNSUPPORTED),  # moved needs 2^k square
+    (hb.hilberta_config(8, 16, 0, 16, 4, 2, 2, 1), hb.HILBERTA_EUNSUPPORTED),  # moved needs a square
     (hb.hilberta_config(8, 8, 0, 7, 2, 0, 0), hb.HILBERTA_EUNSUPPORTED),     # tile does not divide
     (hb.hilberta_config(8, 8, -1, 16, 2, 0, 0), hb.HILBERTA_EINVAL),         # negative text
     (hb.hilberta_config(8, 8, 0, 16, -2, 0, 0), hb.HILBERTA_EINVAL),         # negative delta
@@ -88,7 +91,10 @@ def test_schedule_rejects_bad_configs(lib, cfg, rc):
                                     osched.Layout(16, 16, 0, 60, 15, 4, 4, moved=True),
                                     osched.Layout(8, 8, 3, 15, 4, 2, 2, moved=True),
                                     osched.Layout(64, 64, 512, 1023, 341, 2, 2, moved=True),
-                                    osched.Layout(16, 16, 5, 64, 16, moved=True)])
+                                    osched.Layout(16, 16, 5, 64, 16, moved=True),
+                                    osched.Layout(5, 7, 0, 16, 4, 1, 3),
+                                    osched.Layout(96, 96, 512, 1024, 512, 16, 16),
+                                    osched.Layout(1, 1, 2, 4, 1)])
 def test_schedule_words_match_documented_layout(layout):
     cfg = hb.hilberta_config(layout.grid_h, layout.grid_w, layout.n_txt, layout.tile,
                              layout.delta, layout.shared_h, layout.shared_w, int(layout.moved))
@@ -148,7 +154,7 @@ def test_attention_argument_errors(lib):
     assert attn(lib, qs=hb._STR4(2 * 256 * 64, 256 * 64, 66, 1)) == hb.HILBERTA_EUNSUPPORTED
     assert attn(lib, qs=hb._STR4(2 * 256 * 64, 256 * 64, 64, 2)) == hb.HILBERTA_EUNSUPPORTED
     assert attn(lib, ws=None, wsb=64) == hb.HILBERTA_EINVAL
-    assert attn(lib, cfg=hb.hilberta_config(6, 6, 0, 4, 2, 0, 0)) == hb.HILBERTA_EUNSUPPORTED
+    assert attn(lib, cfg=hb.hilberta_config(6, 6, 0, 7, 2, 0, 0)) == hb.HILBERTA_EUNSUPPORTED  # 7 does not divide 8x8
     assert "scale" in (attn(lib, scale=-1.0) and hb.last_error())
 
 
@@ -182,3 +188,8 @@ def test_permute_errors(lib):
     neg = list(args)
     neg[4] = -1
     assert lib.hilberta_unpermute(*neg, hb.HILBERTA_F32, None) == hb.HILBERTA_EINVAL
+
+
+@pytest.mark.parametrize("h,w", [(1, 1), (2, 2), (3, 5), (96, 96), (128, 128), (129, 3), (1, 32768)])
+def test_image_span_matches_the_oracle(h, w):
+    assert hb.image_span(h, w) == osched.Layout(h, w, 0, 1, 0).n_img

@@ -53,7 +53,9 @@ class Resident:
     def __init__(self, name, dev):
         self.w = w = synth.WORKLOADS[name]
         self.layout = layout_of(w)
-        self.q, self.k, self.v = synth.qkv(w.batch, w.heads, w.n_tot, w.head_dim, w.dtype, seed=w.seed)
+        # the attention sequence: text and the image span (padding included)
+        self.q, self.k, self.v = synth.qkv(w.batch, w.heads, self.layout.n_tot, w.head_dim, w.dtype,
+                                           seed=w.seed)
         self.dev = dev
         self.qd, self.kd, self.vd = (t.to(dev) for t in (self.q, self.k, self.v))
         self.o = torch.empty_like(self.qd)

@@ -76,17 +76,25 @@ def test_strided_rows(gpu):
     assert np.all(out[:, :, c:].cpu().numpy() == 0)
 
 
-def test_rows_with_out_of_range_indices_are_skipped(gpu):
-    n, c = 16, 8
-    x = torch.arange(n * c, dtype=torch.float32, device=gpu).reshape(1, n, c)
+@pytest.mark.parametrize("c", [8, 1024])
+def test_padding_and_out_of_range_entries(gpu, c):
+    # a negative entry is a padding slot: the gather writes a zero row and the
+    # scatter skips it; an entry >= n is skipped by both (flat and row kernels)
+    n = 16
+    x = torch.arange(n * c, dtype=torch.float32, device=gpu).reshape(1, n, c) + 1
     perm = torch.tensor([3, -1, 0, 99] + list(range(4, 16)), dtype=torch.int32, device=gpu)
     y = torch.full_like(x, -5.0)
     hb.hilberta_permute(x, y, perm)
+    back = torch.full_like(x, -6.0)
+    hb.hilberta_unpermute(y, back, perm)
     torch.cuda.synchronize()
-    yc = y.cpu()
-    assert torch.equal(yc[0, 0], x.cpu()[0, 3])
-    assert torch.all(yc[0, 1] == -5.0) and torch.all(yc[0, 3] == -5.0)
-    assert torch.equal(yc[0, 2], x.cpu()[0, 0])
+    yc, xc, bc = y.cpu(), x.cpu(), back.cpu()
+    assert torch.equal(yc[0, 0], xc[0, 3])
+    assert torch.all(yc[0, 1] == 0.0) and torch.all(yc[0, 3] == -5.0)
+    assert torch.equal(yc[0, 2], xc[0, 0])
+    assert torch.equal(bc[0, 3], xc[0, 3]) and torch.equal(bc[0, 0], xc[0, 0])
+    assert torch.all(bc[0, 1] == -6.0) and torch.all(bc[0, 2] == -6.0)
+    assert torch.equal(bc[0, 4:], xc[0, 4:])
 
 
 def test_flux_128_hidden_states(gpu):
