@@ -112,7 +112,10 @@ __device__ __forceinline__ int32_t list_seq(int32_t v, int32_t b1, int32_t b2, i
     return sb + (v - b3);
 }
 
-template <int D>
+// PAD: the image span holds padding positions (a general shape).  A
+// separate instantiation, so that the square power-of-two path carries none
+// of the padding logic.
+template <int D, bool PAD>
 __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
     using G = Geo<D>;
     __shared__ Smem<D> sm;
@@ -185,11 +188,12 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
         sb = a.n_txt;
     }
     const int nblk = (total + kBN - 1) / kBN;
-    const RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
+    RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
+    if (!PAD) ri.pad = false;
 
     const int32_t bb = bh / a.heads;
     const int32_t hh = bh - bb * a.heads;
-    if (a.padded && !dense && !__syncthreads_or(ri.store && !ri.pad)) {
+    if (PAD && !dense && !__syncthreads_or(ri.store && !ri.pad)) {
         // nothing but padding rows (and rows stored elsewhere): no keys
         f32x16 zero[D / 32];
 #pragma unroll
@@ -240,6 +244,28 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
         else if (v0 >= b2 && v0 + cnt <= b3) base = sa + (v0 - b2);
         else if (v0 >= b3) base = sb + (v0 - b3);
         const uint32_t kl = klds0 + buf * G::STAGEB, vl = vlds0 + buf * G::STAGEB;
+        if (PAD) {
+            // every wavefront classifies the stage's keys (lane = key), so
+            // each knows without a barrier whether the stage holds any key
+            // at all; wavefront 0 publishes the per-key masks
+            const int32_t v = v0 + lane;
+            int32_t inf = kKeyInvalid;
+            if (v < total) {
+                const int32_t seq = base >= 0 ? base + lane : list_seq(v, b1, b2, b3, s0, sa, sb, sm.sp);
+                if (!seq_padding(a, seq)) {
+                    inf = kKeyAll;
+                    if (label_mask && v >= b2 && !is_shared_seq(sm.sp, seq))
+                        inf = tile_label(seq - a.n_txt, o, a.tile, a.n_img);
+                }
+            }
+            const bool none = __builtin_amdgcn_ballot_w64(inf != kKeyInvalid) == 0;
+            if (wave == 0) {
+                sm.info[buf][lane] = inf;
+                const bool slow = __builtin_amdgcn_ballot_w64(inf != kKeyAll) != 0;
+                if (lane == 0) sm.slow[buf] = none ? 2 : slow ? 1 : 0;
+            }
+            if (none) return;  // nothing but padding: not loaded, not computed
+        }
         if (base >= 0 && cnt == kBN) {
             // a full stage of contiguous keys: one uniform offset
             const int32_t kb0 = base * krow_b, vb0 = base * vrow_b;
@@ -258,23 +284,7 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
                 dma16(vrs, vl + j * 1024, key * vrow_b + vcol[j]);
             }
         }
-        if (a.padded) {
-            if (tid < kBN) {
-                const int32_t v = v0 + tid;
-                int32_t inf = kKeyInvalid;
-                if (v < total) {
-                    const int32_t seq = base >= 0 ? base + tid : list_seq(v, b1, b2, b3, s0, sa, sb, sm.sp);
-                    if (!seq_padding(a, seq)) {
-                        inf = kKeyAll;
-                        if (label_mask && v >= b2 && !is_shared_seq(sm.sp, seq))
-                            inf = tile_label(seq - a.n_txt, o, a.tile, a.n_img);
-                    }
-                }
-                sm.info[buf][tid] = inf;
-                const bool slow = __builtin_amdgcn_ballot_w64(inf != kKeyAll) != 0;
-                if (tid == 0) sm.slow[buf] = slow;
-            }
-        } else if (!stage_fast(i) && tid < kBN) {
+        if (!PAD && !stage_fast(i) && tid < kBN) {
             const int32_t v = v0 + tid;
             int32_t inf = kKeyInvalid;
             if (v < total) {
@@ -317,86 +327,90 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
     for (int32_t i = 0; i < nblk; ++i) {
         const int buf = i & 1;
         if (i + 1 < nblk) load_stage(i + 1, buf ^ 1);
-        const uint8_t* kb_ = sm.k[buf];
-        const uint8_t* vb_ = sm.v[buf];
+        // padded spans: sm.slow is 0 (no masks), 1 (per-key masks) or 2
+        // (only padding keys: the stage is skipped)
+        if (!PAD || sm.slow[buf] != 2) {
+            const uint8_t* kb_ = sm.k[buf];
+            const uint8_t* vb_ = sm.v[buf];
 
-        // S^T: s[kt] register e holds key 32 kt + 8 (e/4) + 4 h + e%4.  All
-        // K operands are requested first, so the MFMAs only wait for the
-        // first ones to arrive.
-        bf16x8 kop[D / 16][2];
+            // S^T: s[kt] register e holds key 32 kt + 8 (e/4) + 4 h + e%4.  All
+            // K operands are requested first, so the MFMAs only wait for the
+            // first ones to arrive.
+            bf16x8 kop[D / 16][2];
 #pragma unroll
-        for (int kc = 0; kc < D / 16; ++kc)
+            for (int kc = 0; kc < D / 16; ++kc)
 #pragma unroll
-            for (int kt = 0; kt < 2; ++kt)
-                kop[kc][kt] = *reinterpret_cast<const bf16x8*>(kb_ + (ka ^ (32 * kc)) + kt * 32 * G::ROWB);
-        __builtin_amdgcn_sched_barrier(0);
-        f32x16 s[2] = {f32x16{}, f32x16{}};
+                for (int kt = 0; kt < 2; ++kt)
+                    kop[kc][kt] = *reinterpret_cast<const bf16x8*>(kb_ + (ka ^ (32 * kc)) + kt * 32 * G::ROWB);
+            __builtin_amdgcn_sched_barrier(0);
+            f32x16 s[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-        for (int kc = 0; kc < D / 16; ++kc)
+            for (int kc = 0; kc < D / 16; ++kc)
 #pragma unroll
-            for (int kt = 0; kt < 2; ++kt)
-                s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kc][kt], q[kc], s[kt], 0, 0, 0);
-        // V^T operands of the whole stage, in flight during the softmax
-        bf16x8 vop[4][D / 32];
+                for (int kt = 0; kt < 2; ++kt)
+                    s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kc][kt], q[kc], s[kt], 0, 0, 0);
+            // V^T operands of the whole stage, in flight during the softmax
+            bf16x8 vop[4][D / 32];
 #pragma unroll
-        for (int cc = 0; cc < 4; ++cc)
+            for (int cc = 0; cc < 4; ++cc)
 #pragma unroll
-            for (int dt = 0; dt < D / 32; ++dt) {
-                const uint8_t* vp = vb_ + (va ^ (64 * dt)) + 16 * cc * G::ROWB;
-                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vp));
-                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vp + 8 * G::ROWB));
-                vop[cc][dt] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-            }
-        __builtin_amdgcn_sched_barrier(0);
-        if (a.padded ? sm.slow[buf] != 0 : !stage_fast(i)) {
-#pragma unroll
-            for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int32_t inf = sm.info[buf][32 * kt + 8 * (e >> 2) + 4 * h + (e & 3)];
-                    s[kt][e] = (inf == kKeyAll || inf == ri.label) ? s[kt][e] : -INFINITY;
+                for (int dt = 0; dt < D / 32; ++dt) {
+                    const uint8_t* vp = vb_ + (va ^ (64 * dt)) + 16 * cc * G::ROWB;
+                    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vp));
+                    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vp + 8 * G::ROWB));
+                    vop[cc][dt] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
                 }
-        }
-        // row max over the 64 keys: a tree of three-way maxima
-        float t3[11];
+            __builtin_amdgcn_sched_barrier(0);
+            if (PAD ? sm.slow[buf] != 0 : !stage_fast(i)) {
 #pragma unroll
-        for (int g = 0; g < 5; ++g) {
-            t3[g] = fmaxf(fmaxf(s[0][3 * g], s[0][3 * g + 1]), s[0][3 * g + 2]);
-            t3[5 + g] = fmaxf(fmaxf(s[1][3 * g], s[1][3 * g + 1]), s[1][3 * g + 2]);
-        }
-        t3[10] = fmaxf(s[0][15], s[1][15]);
-        const float u0 = fmaxf(fmaxf(t3[0], t3[1]), t3[2]);
-        const float u1 = fmaxf(fmaxf(t3[3], t3[4]), t3[5]);
-        const float u2 = fmaxf(fmaxf(t3[6], t3[7]), t3[8]);
-        const float u3 = fmaxf(t3[9], t3[10]);
-        const float mx = half_max(fmaxf(fmaxf(u0, u1), fmaxf(u2, u3))) * c;
-        if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f)) {
-            const float m_new = fmaxf(m_run, mx);
-            // a row with every key masked so far keeps -inf: leave it alone
-            const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-            m_run = m_new;
+                for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-            for (int x = 0; x < 4; ++x) lp[x] *= alpha;
-#pragma unroll
-            for (int dt = 0; dt < D / 32; ++dt) acc[dt] *= alpha;
-        }
-        const float m_use = m_run == -INFINITY ? 0.f : m_run;
-        // P = exp2(S c - m) rounded to bf16; chunk cc of 16 keys holds key
-        // 16 cc + 8 (j/4) + 4 h + j%4 in register j
-        bf16x8 p[4];
-#pragma unroll
-        for (int cc = 0; cc < 4; ++cc)
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const float pe = __builtin_amdgcn_exp2f(fmaf(s[cc >> 1][8 * (cc & 1) + j], c, -m_use));
-                lp[cc] += pe;
-                p[cc][j] = (__bf16)pe;
+                    for (int e = 0; e < 16; ++e) {
+                        const int32_t inf = sm.info[buf][32 * kt + 8 * (e >> 2) + 4 * h + (e & 3)];
+                        s[kt][e] = (inf == kKeyAll || inf == ri.label) ? s[kt][e] : -INFINITY;
+                    }
             }
+            // row max over the 64 keys: a tree of three-way maxima
+            float t3[11];
 #pragma unroll
-        for (int cc = 0; cc < 4; ++cc)
+            for (int g = 0; g < 5; ++g) {
+                t3[g] = fmaxf(fmaxf(s[0][3 * g], s[0][3 * g + 1]), s[0][3 * g + 2]);
+                t3[5 + g] = fmaxf(fmaxf(s[1][3 * g], s[1][3 * g + 1]), s[1][3 * g + 2]);
+            }
+            t3[10] = fmaxf(s[0][15], s[1][15]);
+            const float u0 = fmaxf(fmaxf(t3[0], t3[1]), t3[2]);
+            const float u1 = fmaxf(fmaxf(t3[3], t3[4]), t3[5]);
+            const float u2 = fmaxf(fmaxf(t3[6], t3[7]), t3[8]);
+            const float u3 = fmaxf(t3[9], t3[10]);
+            const float mx = half_max(fmaxf(fmaxf(u0, u1), fmaxf(u2, u3))) * c;
+            if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f)) {
+                const float m_new = fmaxf(m_run, mx);
+                // a row with every key masked so far keeps -inf: leave it alone
+                const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+                m_run = m_new;
 #pragma unroll
-            for (int dt = 0; dt < D / 32; ++dt)
-                acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[cc][dt], p[cc], acc[dt], 0, 0, 0);
+                for (int x = 0; x < 4; ++x) lp[x] *= alpha;
+#pragma unroll
+                for (int dt = 0; dt < D / 32; ++dt) acc[dt] *= alpha;
+            }
+            const float m_use = m_run == -INFINITY ? 0.f : m_run;
+            // P = exp2(S c - m) rounded to bf16; chunk cc of 16 keys holds key
+            // 16 cc + 8 (j/4) + 4 h + j%4 in register j
+            bf16x8 p[4];
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const float pe = __builtin_amdgcn_exp2f(fmaf(s[cc >> 1][8 * (cc & 1) + j], c, -m_use));
+                    lp[cc] += pe;
+                    p[cc][j] = (__bf16)pe;
+                }
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+                for (int dt = 0; dt < D / 32; ++dt)
+                    acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[cc][dt], p[cc], acc[dt], 0, 0, 0);
+        }
         // stage i+1 must have landed before anyone reads it, and every
         // wavefront must be done with this buffer before it is refilled
         wait_vmcnt<0>();
@@ -410,7 +424,10 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
 
 template <int D>
 hipError_t launch_t(const AttnArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL((attn_bf16_kernel<D>), dim3(a.total_items), dim3(kThreads), 0, s, a);
+    if (a.padded)
+        hipLaunchKernelGGL((attn_bf16_kernel<D, true>), dim3(a.total_items), dim3(kThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL((attn_bf16_kernel<D, false>), dim3(a.total_items), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 
