@@ -17,6 +17,8 @@ Everything here is slow and obviously correct on purpose:
                     and the schedule table in the library's documented layout.
 * ``attention``  -- masked softmax attention in float64 from its closed
                     form, plus a pure-Python loop version for tiny inputs.
+* ``gradients``  -- dQ, dK, dV of the masked attention by the chain rule
+                    (the backward pass training needs).
 * ``tokens``     -- the token gather / scatter of §3.4.
 * ``accounting`` -- nnz of the mask and the FLOP count of §4.2.
 
@@ -24,4 +26,4 @@ No function shares code, tables or constants with the HIP path; the two meet
 only on seeded inputs produced elsewhere.
 """
 
-from . import hilbert, schedule, attention, tokens, accounting  # noqa: F401
+from . import hilbert, schedule, attention, gradients, tokens, accounting  # noqa: F401

@@ -12,12 +12,13 @@ import math
 import numpy as np
 import pytest
 
-from oracle import accounting, attention, hilbert, schedule, tokens
+from oracle import accounting, attention, gradients, hilbert, schedule, tokens
 from oracle.schedule import Layout
 
 import test_oracle_accounting as t_acc
 import test_oracle_attention as t_att
 import test_oracle_general as t_gen
+import test_oracle_gradients as t_grad
 import test_oracle_hilbert as t_hil
 import test_oracle_moved as t_mov
 import test_oracle_schedule as t_sch
@@ -55,6 +56,8 @@ PINS = [
     lambda: t_gen.test_shared_region_is_centred_in_the_grid(),
     lambda: t_gen.test_padded_sequence_equals_raster_construction(t_gen.PADDED[1], 1),
     lambda: t_gen.test_padding_content_does_not_reach_other_rows(t_gen.PADDED[0]),
+    lambda: t_grad.test_finite_differences(t_grad.LAYOUTS[0], 1),
+    lambda: t_grad.test_matches_torch_autograd(t_grad.LAYOUTS[3], 1),
 ]
 
 
@@ -194,6 +197,31 @@ def _region_centred_in_enclosing_grid(orig):
     return f
 
 
+def _grads_with(mistake):
+    """masked_attention_grads with one planted mistake."""
+    def f(q, k, v, do, mask_fn, scale=None, block=512):
+        q, k, v, do = (np.asarray(a, dtype=np.float64) for a in (q, k, v, do))
+        b, h, n, d = q.shape
+        scale = 1.0 / math.sqrt(d) if scale is None else scale
+        rows = np.arange(n)
+        m = mask_fn(rows)
+        some = m.any(axis=1)
+        s = np.where(m[None, None], np.einsum("bhid,bhjd->bhij", q, k) * scale, -np.inf)
+        mx = np.where(some[None, None, :, None], s.max(axis=-1, keepdims=True), 0.0)
+        e = np.exp(s - mx)
+        den = e.sum(axis=-1, keepdims=True)
+        p = e / np.where(den > 0, den, 1.0)
+        o = np.einsum("bhij,bhjd->bhid", p, v)
+        dlt = np.sum(do * o, axis=-1, keepdims=True)
+        dp = np.einsum("bhid,bhjd->bhij", do, v)
+        ds = p * dp if mistake == "no_row_term" else p * (dp - dlt)
+        dq = (1.0 if mistake == "dq_unscaled" else scale) * np.einsum("bhij,bhjd->bhid", ds, k)
+        dk = scale * np.einsum("bhij,bhid->bhjd", ds, k if mistake == "dk_from_k" else q)
+        dv = np.einsum("bhij,bhid->bhjd", e if mistake == "dv_unnormalised" else p, do)
+        return dq, dk, dv
+    return lambda orig: f
+
+
 MUTANTS = {
     "curve transposed": (hilbert, "xy_iterative", _xy_transposed),
     "curve without reflection": (hilbert, "xy_iterative", _xy_no_reflection),
@@ -214,6 +242,10 @@ MUTANTS = {
     "padding attended as keys and queries": (schedule, "token_valid", _padding_keys_valid),
     "general grid transposed": (hilbert, "padded_perm", _padded_grid_transposed),
     "region centred in the enclosing grid": (schedule, "shared_raster", _region_centred_in_enclosing_grid),
+    "gradient without the row term": (gradients, "masked_attention_grads", _grads_with("no_row_term")),
+    "dQ without the scale": (gradients, "masked_attention_grads", _grads_with("dq_unscaled")),
+    "dK from K instead of Q": (gradients, "masked_attention_grads", _grads_with("dk_from_k")),
+    "dV from unnormalised P": (gradients, "masked_attention_grads", _grads_with("dv_unnormalised")),
     "moved prefix without the shared tokens": (
         Layout, "prefix", lambda orig: property(lambda self: self.n_txt)),
 }
