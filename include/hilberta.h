@@ -236,6 +236,64 @@ int hilberta_attn_fwd(const hilberta_config* cfg, const int32_t* sched,
                       const int64_t o_strides[4], int dtype, float scale,
                       void* workspace, int64_t workspace_bytes, void* stream);
 
+/*
+ * hilberta_attn_bwd_workspace_bytes -- device workspace hilberta_attn_bwd
+ * needs: 8 bytes per row of every (batch, head), for dO . O and the LSE in
+ * log2 units.  Host only.  Errors: as hilberta_schedule_words for cfg;
+ * EUNSUPPORTED (head_dim, dtype other than bf16).
+ */
+int hilberta_attn_bwd_workspace_bytes(const hilberta_config* cfg, int64_t batch,
+                                      int64_t heads, int64_t head_dim, int dtype,
+                                      int64_t* bytes);
+
+/*
+ * hilberta_attn_bwd -- gradients of hilberta_attn_fwd's output with respect
+ * to Q, K and V (the backward pass that training through the sparse
+ * attention needs: §4.1 fine-tunes with LoRA, the appendix on training
+ * from scratch trains a DiT).  For every (batch, head), with P the forward's
+ * probabilities (masked entries 0) and dO the gradient of O:
+ *   dV = P^T dO,  dP = dO V^T,  dS = P (dP - rowsum(dO * O)),
+ *   dQ = scale dS K,  dK = scale dS^T Q.
+ * Padding slots of a general shape get zero gradients.
+ *   sched      the table the forward used (same cfg and layer).
+ *   q,k,v,o    the forward's inputs and output; dout shares o's strides,
+ *              dq q's, dk k's and dv v's; all [batch, heads, N_tot, head_dim]
+ *              device tensors as for hilberta_attn_fwd; dq, dk, dv are
+ *              written completely and may not overlap the inputs.
+ *   lse        the forward's natural-log LSE, device float[batch*heads*N_tot].
+ *   dtype      HILBERTA_BF16 only: bf16 tensors, fp32 accumulation, P and dS
+ *              rounded to bf16 as matrix operands.
+ *   scale      the forward's softmax scale.
+ *   workspace  device scratch of at least hilberta_attn_bwd_workspace_bytes
+ *              (required), 16-byte aligned.
+ * Deterministic: every gradient row is written once, without atomics.
+ * Errors: EINVAL (NULL pointers, no workspace), EUNSUPPORTED (head_dim,
+ * dtype, stride alignment), ECAPACITY (workspace too small), EHIP.
+ */
+int hilberta_attn_bwd(const hilberta_config* cfg, const int32_t* sched,
+                      const void* q, const void* k, const void* v, const void* o,
+                      const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                      int64_t batch, int64_t heads, int64_t head_dim,
+                      const int64_t q_strides[4], const int64_t k_strides[4],
+                      const int64_t v_strides[4], const int64_t o_strides[4], int dtype,
+                      float scale, void* workspace, int64_t workspace_bytes, void* stream);
+
+/* dense_attn_bwd_workspace_bytes -- workspace for dense_attn_bwd. Host only. */
+int dense_attn_bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n,
+                                   int64_t head_dim, int dtype, int64_t* bytes);
+
+/*
+ * dense_attn_bwd -- gradients of dense_attn_fwd (the baseline the sparse
+ * backward is measured against).  Arguments as for hilberta_attn_bwd with
+ * N_tot = n and no schedule.
+ */
+int dense_attn_bwd(const void* q, const void* k, const void* v, const void* o,
+                   const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                   int64_t batch, int64_t heads, int64_t n, int64_t head_dim,
+                   const int64_t q_strides[4], const int64_t k_strides[4],
+                   const int64_t v_strides[4], const int64_t o_strides[4], int dtype,
+                   float scale, void* workspace, int64_t workspace_bytes, void* stream);
+
 /* dense_attn_workspace_bytes -- workspace for dense_attn_fwd. Host only. */
 int dense_attn_workspace_bytes(int64_t batch, int64_t heads, int64_t n,
                                int64_t head_dim, int dtype, int64_t* bytes);

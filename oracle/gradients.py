@@ -55,3 +55,50 @@ def masked_attention_grads(q, k, v, do, mask_fn, scale=None, block=512):
         dk += scale * np.einsum("bhij,bhid->bhjd", ds, q[:, :, rows])
         dv += np.einsum("bhij,bhid->bhjd", p, do[:, :, rows])
     return dq, dk, dv
+
+
+def masked_attention_grads_rows(q, k, v, do, mask_fn, q_rows, k_rows, scale=None, block=512):
+    """Selected rows of the gradients, for problems too large for the full
+    matrices: dQ at the query rows q_rows, dK and dV at the key rows k_rows
+    (float64, [B, H, len(rows), D]).  Same formulas as
+    ``masked_attention_grads``; the key rows' sums run over every query row
+    that attends them, each with its own full softmax row."""
+    q, k, v, do = (np.asarray(a, dtype=np.float64) for a in (q, k, v, do))
+    b, h, n, d = q.shape
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    q_rows = np.asarray(q_rows, dtype=np.int64)
+    k_rows = np.asarray(k_rows, dtype=np.int64)
+
+    def rows_softmax(rows, m):
+        some = m.any(axis=1)
+        s = np.matmul(q[:, :, rows], np.swapaxes(k, -1, -2)) * scale
+        s = np.where(m[None, None], s, -np.inf)
+        mx = np.where(some[None, None, :, None], s.max(axis=-1, keepdims=True), 0.0)
+        p = np.exp(s - mx)
+        den = p.sum(axis=-1, keepdims=True)
+        p = p / np.where(den > 0, den, 1.0)
+        dlt = np.sum(do[:, :, rows] * np.matmul(p, v), axis=-1, keepdims=True)
+        return p, dlt
+
+    dq = np.zeros((b, h, q_rows.size, d))
+    for r0 in range(0, q_rows.size, block):
+        rows = q_rows[r0:r0 + block]
+        p, dlt = rows_softmax(rows, mask_fn(rows))
+        ds = p * (np.matmul(do[:, :, rows], np.swapaxes(v, -1, -2)) - dlt)
+        dq[:, :, r0:r0 + rows.size] = scale * np.matmul(ds, k)
+    dk = np.zeros((b, h, k_rows.size, d))
+    dv = np.zeros((b, h, k_rows.size, d))
+    for r0 in range(0, n, block):
+        rows = np.arange(r0, min(n, r0 + block))
+        m = mask_fn(rows)
+        att = m[:, k_rows].any(axis=1)
+        if not att.any():
+            continue
+        rows, m = rows[att], m[att]
+        p, dlt = rows_softmax(rows, m)
+        pk = p[..., k_rows]
+        ds = pk * (np.matmul(do[:, :, rows], np.swapaxes(v[:, :, k_rows], -1, -2)) - dlt)
+        dk += scale * np.matmul(np.swapaxes(ds, -1, -2), q[:, :, rows])
+        dv += np.matmul(np.swapaxes(pk, -1, -2), do[:, :, rows])
+    return dq, dk, dv

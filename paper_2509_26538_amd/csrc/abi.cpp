@@ -209,17 +209,15 @@ Plan make_plan(bool sparse, int64_t n_txt, int64_t n_img, int64_t n_shared, int6
     return p;
 }
 
-int run_attention(bool sparse, const hilberta_config* cfg, const int32_t* sched, const void* q,
-                  const void* k, const void* v, void* o, float* lse, int64_t batch, int64_t heads,
-                  int64_t n_tot, int64_t head_dim, const int64_t* qs, const int64_t* ks,
-                  const int64_t* vs, const int64_t* os, int dtype, float scale, void* ws,
-                  int64_t ws_bytes, void* stream) {
-    const Tensor4 t[4] = {{q, qs, "q"}, {k, ks, "k"}, {v, vs, "v"}, {o, os, "o"}};
-    int rc = check_attn_common(t, 4, batch, heads, n_tot, head_dim, dtype, scale);
+// Validates what the forward and the backward share (tensors t, shapes,
+// dtype, scale) and builds the launch description.  Returns OK with *empty
+// set when there is nothing to read or write.
+int attn_setup(bool sparse, const hilberta_config* cfg, const int32_t* sched, const Tensor4* t, int n_t,
+               int64_t batch, int64_t heads, int64_t n_tot, int64_t head_dim, int dtype, float scale,
+               bool allow_split, Plan& p, hilberta::AttnArgs& a, bool& empty) {
+    empty = false;
+    int rc = check_attn_common(t, n_t, batch, heads, n_tot, head_dim, dtype, scale);
     if (rc) return rc;
-    if (ws_bytes < 0 || (ws == nullptr && ws_bytes != 0))
-        return fail(HILBERTA_EINVAL, "workspace NULL with %lld bytes", (long long)ws_bytes);
-    if (ws && (uintptr_t)ws % 16) return fail(HILBERTA_EUNSUPPORTED, "workspace is not 16-byte aligned");
     // the attention sees a global prefix and a tiled span (see Geom)
     int64_t n_txt = 0, n_img = n_tot, n_shared = 0, tile = n_tot, n_tiles = 1, cap = 0;
     if (sparse) {
@@ -232,31 +230,35 @@ int run_attention(bool sparse, const hilberta_config* cfg, const int32_t* sched,
         cap = g.cap;
     }
     if (n_tot > 0x7fffffffLL) return fail(HILBERTA_EUNSUPPORTED, "sequence too long");
-    {
-        // K and V rows of one (batch, head) are addressed with 32-bit byte
-        // offsets from the slice's base
-        const int64_t es = dtype == HILBERTA_BF16 ? 2 : 4;
-        const int64_t rs = ks[2] > vs[2] ? ks[2] : vs[2];
-        if (((n_tot - 1) * rs + head_dim) * es > 0x7fffffffLL)
-            return fail(HILBERTA_EUNSUPPORTED, "one (batch, head) slice of K or V spans more than 2 GiB");
-        if (ks[2] < head_dim || vs[2] < head_dim)
-            return fail(HILBERTA_EINVAL, "K/V row stride smaller than head_dim");
-    }
     const int64_t bh = batch * heads;
-    if (bh == 0 || n_tot == 0) return HILBERTA_OK;
-    Plan p = make_plan(sparse, n_txt, n_img, n_shared, tile, n_tot, bh, head_dim, dtype, ws != nullptr);
-    if (ws && ws_bytes < p.ws_bytes)
-        return fail(HILBERTA_ECAPACITY, "workspace of %lld bytes, %lld needed", (long long)ws_bytes,
-                    (long long)p.ws_bytes);
+    if (bh == 0 || n_tot == 0) {
+        empty = true;
+        return HILBERTA_OK;
+    }
+    {
+        // rows staged through LDS are addressed with 32-bit byte offsets
+        // from their (batch, head) slice's base: K and V, and for the
+        // backward Q and dO too (t[4] is dO, which shares O's strides)
+        const int64_t es = dtype == HILBERTA_BF16 ? 2 : 4;
+        int64_t rs = 0;
+        for (int i = 0; i < n_t; ++i) {
+            if (t[i].s[2] < head_dim) return fail(HILBERTA_EINVAL, "%s: row stride smaller than head_dim", t[i].name);
+            if (i == 1 || i == 2 || n_t > 4) rs = t[i].s[2] > rs ? t[i].s[2] : rs;
+        }
+        if (((n_tot - 1) * rs + head_dim) * es > 0x7fffffffLL)
+            return fail(HILBERTA_EUNSUPPORTED, "one (batch, head) slice of a staged tensor spans more than 2 GiB");
+    }
+    p = make_plan(sparse, n_txt, n_img, n_shared, tile, n_tot, bh, head_dim, dtype, allow_split);
     if (p.total_items > 0x7fffffffLL) return fail(HILBERTA_EUNSUPPORTED, "too many work items");
-
-    hilberta::AttnArgs a{};
-    a.q = q;
-    a.k = k;
-    a.v = v;
-    a.o = o;
-    a.lse = lse;
-    a.ws = static_cast<float*>(ws);
+    const int64_t* qs = t[0].s;
+    const int64_t* ks = t[1].s;
+    const int64_t* vs = t[2].s;
+    const int64_t* os = t[3].s;
+    a = hilberta::AttnArgs{};
+    a.q = t[0].p;
+    a.k = t[1].p;
+    a.v = t[2].p;
+    a.o = const_cast<void*>(t[3].p);
     a.sched = sched;
     a.q_sb = qs[0]; a.q_sh = qs[1]; a.q_sr = qs[2];
     a.k_sb = ks[0]; a.k_sh = ks[1]; a.k_sr = ks[2];
@@ -286,6 +288,35 @@ int run_attention(bool sparse, const hilberta_config* cfg, const int32_t* sched,
         a.grid_h = cfg->grid_h;
         a.grid_w = cfg->grid_w;
     }
+    return HILBERTA_OK;
+}
+
+int check_workspace(const void* ws, int64_t ws_bytes) {
+    if (ws_bytes < 0 || (ws == nullptr && ws_bytes != 0))
+        return fail(HILBERTA_EINVAL, "workspace NULL with %lld bytes", (long long)ws_bytes);
+    if (ws && (uintptr_t)ws % 16) return fail(HILBERTA_EUNSUPPORTED, "workspace is not 16-byte aligned");
+    return HILBERTA_OK;
+}
+
+int run_attention(bool sparse, const hilberta_config* cfg, const int32_t* sched, const void* q,
+                  const void* k, const void* v, void* o, float* lse, int64_t batch, int64_t heads,
+                  int64_t n_tot, int64_t head_dim, const int64_t* qs, const int64_t* ks,
+                  const int64_t* vs, const int64_t* os, int dtype, float scale, void* ws,
+                  int64_t ws_bytes, void* stream) {
+    const Tensor4 t[4] = {{q, qs, "q"}, {k, ks, "k"}, {v, vs, "v"}, {o, os, "o"}};
+    int rc = check_workspace(ws, ws_bytes);
+    if (rc) return rc;
+    Plan p{};
+    hilberta::AttnArgs a{};
+    bool empty = false;
+    rc = attn_setup(sparse, cfg, sched, t, 4, batch, heads, n_tot, head_dim, dtype, scale, ws != nullptr, p, a,
+                    empty);
+    if (rc || empty) return rc;
+    if (ws && ws_bytes < p.ws_bytes)
+        return fail(HILBERTA_ECAPACITY, "workspace of %lld bytes, %lld needed", (long long)ws_bytes,
+                    (long long)p.ws_bytes);
+    a.lse = lse;
+    a.ws = static_cast<float*>(ws);
     hipStream_t s = static_cast<hipStream_t>(stream);
     rc = hip_status(hilberta::launch_attn(a, dtype, (int)head_dim, s), "attention launch");
     if (rc || p.n_chunks == 1) return rc;
@@ -297,14 +328,61 @@ int run_attention(bool sparse, const hilberta_config* cfg, const int32_t* sched,
     m.o_sb = os[0]; m.o_sh = os[1]; m.o_sr = os[2];
     m.heads = (int32_t)heads;
     m.n_tot = (int32_t)n_tot;
-    m.n_txt = (int32_t)n_txt;
-    m.span_cap = (int32_t)cap;
+    m.n_txt = a.n_txt;
+    m.span_cap = a.span_cap;
     m.n_dense_rows = (int32_t)p.n_dense_rows;
     m.n_chunks = (int32_t)p.n_chunks;
-    m.n_bh = (int32_t)bh;
-    m.n_tiles = (int32_t)n_tiles;
+    m.n_bh = a.n_bh;
+    m.n_tiles = a.n_tiles;
     m.sparse = a.sparse;
     return hip_status(hilberta::launch_merge(m, dtype, (int)head_dim, s), "merge launch");
+}
+
+// Workspace of the backward: dO . O and the base-2 LSE per row.
+int64_t bwd_ws_bytes(int64_t bh, int64_t n_tot) { return bh * n_tot * 2 * 4; }
+
+int run_attention_bwd(bool sparse, const hilberta_config* cfg, const int32_t* sched, const void* q,
+                      const void* k, const void* v, const void* o, const void* dout, const float* lse,
+                      void* dq, void* dk, void* dv, int64_t batch, int64_t heads, int64_t n_tot,
+                      int64_t head_dim, const int64_t* qs, const int64_t* ks, const int64_t* vs,
+                      const int64_t* os, int dtype, float scale, void* ws, int64_t ws_bytes, void* stream) {
+    const Tensor4 t[8] = {{q, qs, "q"},       {k, ks, "k"},   {v, vs, "v"},   {o, os, "o"},
+                          {dout, os, "dout"}, {dq, qs, "dq"}, {dk, ks, "dk"}, {dv, vs, "dv"}};
+    int rc = check_workspace(ws, ws_bytes);
+    if (rc) return rc;
+    if (dtype != HILBERTA_BF16 && dtype != HILBERTA_F32) return fail(HILBERTA_EUNSUPPORTED, "dtype %d", dtype);
+    if (dtype != HILBERTA_BF16) return fail(HILBERTA_EUNSUPPORTED, "the backward runs in bf16 only");
+    Plan p{};
+    hilberta::AttnArgs a{};
+    bool empty = false;
+    rc = attn_setup(sparse, cfg, sched, t, 8, batch, heads, n_tot, head_dim, dtype, scale, false, p, a, empty);
+    if (rc || empty) return rc;
+    if (!lse) return fail(HILBERTA_EINVAL, "lse is NULL");
+    const int64_t need = bwd_ws_bytes(batch * heads, n_tot);
+    if (!ws) return fail(HILBERTA_EINVAL, "the backward needs a workspace of %lld bytes", (long long)need);
+    if (ws_bytes < need)
+        return fail(HILBERTA_ECAPACITY, "workspace of %lld bytes, %lld needed", (long long)ws_bytes,
+                    (long long)need);
+    hilberta::BwdArgs g{};
+    g.dout = dout;
+    g.lse = lse;
+    g.dq = dq;
+    g.dk = dk;
+    g.dv = dv;
+    g.delta = static_cast<float*>(ws);
+    g.lse2 = static_cast<float*>(ws) + batch * heads * n_tot;
+    return hip_status(hilberta::launch_attn_bwd(a, g, (int)head_dim, static_cast<hipStream_t>(stream)),
+                      "backward launch");
+}
+
+int bwd_ws_query(int64_t batch, int64_t heads, int64_t n_tot, int64_t head_dim, int dtype, int64_t* bytes) {
+    if (!bytes) return fail(HILBERTA_EINVAL, "bytes is NULL");
+    if (batch < 0 || heads < 0 || n_tot < 0) return fail(HILBERTA_EINVAL, "negative size");
+    if (head_dim != 64 && head_dim != 128)
+        return fail(HILBERTA_EUNSUPPORTED, "head_dim %lld not in {64, 128}", (long long)head_dim);
+    if (dtype != HILBERTA_BF16) return fail(HILBERTA_EUNSUPPORTED, "the backward runs in bf16 only");
+    *bytes = bwd_ws_bytes(batch * heads, n_tot);
+    return HILBERTA_OK;
 }
 
 int run_permute(bool scatter, const void* x, void* y, const int32_t* perm, int64_t batch, int64_t n,
@@ -449,6 +527,43 @@ int hilberta_attn_fwd(const hilberta_config* cfg, const int32_t* sched, const vo
     return run_attention(true, cfg, sched, q, k, v, o, lse_or_null, batch, heads, n_tot, head_dim,
                          q_strides, k_strides, v_strides, o_strides, dtype, scale, workspace,
                          workspace_bytes, stream);
+}
+
+int hilberta_attn_bwd_workspace_bytes(const hilberta_config* cfg, int64_t batch, int64_t heads,
+                                      int64_t head_dim, int dtype, int64_t* bytes) {
+    int rc = check_config(cfg);
+    if (rc) return rc;
+    return bwd_ws_query(batch, heads, cfg->n_txt + span_len(cfg), head_dim, dtype, bytes);
+}
+
+int hilberta_attn_bwd(const hilberta_config* cfg, const int32_t* sched, const void* q, const void* k,
+                      const void* v, const void* o, const void* dout, const float* lse, void* dq, void* dk,
+                      void* dv, int64_t batch, int64_t heads, int64_t head_dim, const int64_t q_strides[4],
+                      const int64_t k_strides[4], const int64_t v_strides[4], const int64_t o_strides[4],
+                      int dtype, float scale, void* workspace, int64_t workspace_bytes, void* stream) {
+    int rc = check_config(cfg);
+    if (rc) return rc;
+    if (!sched) return fail(HILBERTA_EINVAL, "sched is NULL");
+    const int64_t n_tot = cfg->n_txt + span_len(cfg);
+    return run_attention_bwd(true, cfg, sched, q, k, v, o, dout, lse, dq, dk, dv, batch, heads, n_tot, head_dim,
+                             q_strides, k_strides, v_strides, o_strides, dtype, scale, workspace, workspace_bytes,
+                             stream);
+}
+
+int dense_attn_bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t head_dim, int dtype,
+                                   int64_t* bytes) {
+    return bwd_ws_query(batch, heads, n, head_dim, dtype, bytes);
+}
+
+int dense_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                   const float* lse, void* dq, void* dk, void* dv, int64_t batch, int64_t heads, int64_t n,
+                   int64_t head_dim, const int64_t q_strides[4], const int64_t k_strides[4],
+                   const int64_t v_strides[4], const int64_t o_strides[4], int dtype, float scale,
+                   void* workspace, int64_t workspace_bytes, void* stream) {
+    if (n < 0) return fail(HILBERTA_EINVAL, "n < 0");
+    return run_attention_bwd(false, nullptr, nullptr, q, k, v, o, dout, lse, dq, dk, dv, batch, heads, n, head_dim,
+                             q_strides, k_strides, v_strides, o_strides, dtype, scale, workspace, workspace_bytes,
+                             stream);
 }
 
 int dense_attn_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t head_dim, int dtype,

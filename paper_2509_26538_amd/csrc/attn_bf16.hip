@@ -46,24 +46,10 @@
 // decoded to its cell) and flags the stage for the per-key masks only if a
 // key is padding or needs a label; a query block made of padding rows only
 // stores its empty-softmax rows without visiting any key.
-#include "attn_common.hpp"
+#include "bf16_stage.hpp"
 
 namespace hilberta {
 namespace {
-
-constexpr int kBN = 64;  // keys per stage
-static_assert(kBlockMBf16 == 128, "four wavefronts of 32 rows");
-
-template <int D>
-struct Geo {
-    static constexpr int CPR = D / 8;              // 16-byte chunks per row
-    static constexpr int ROWB = D * 2;             // bytes per row
-    static constexpr int STAGEB = kBN * ROWB;      // bytes per tensor and stage
-    static constexpr int IPW = STAGEB / 1024 / 4;  // 1 KB direct loads per wavefront and tensor
-    // chunk swizzles (XOR on the 16-byte chunk index of a row)
-    __device__ __forceinline__ static int fk(int row) { return D == 128 ? (row & 15) : ((row >> 1) & 7); }
-    __device__ __forceinline__ static int fv(int row) { return D == 128 ? 4 * (row & 3) : 4 * ((row >> 1) & 1); }
-};
 
 template <int D>
 struct Smem {
@@ -74,43 +60,6 @@ struct Smem {
     int32_t n_keep;
     int32_t slow[2];  // padded spans: stage needs the per-key masks
 };
-
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-
-// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt");
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-// One 16-byte-per-lane buffer load straight into LDS at lds_base + 16 lane,
-// bounds-checked against the resource.  Inline assembly, so that the
-// compiler does not guard later LDS reads with a wait for it: the kernel
-// waits for each stage explicitly before the barrier that publishes it.
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rsrc, uint32_t lds_base, int32_t voff) {
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-                 :
-                 : "s"(lds_base), "v"(voff), "s"(rsrc)
-                 : "memory", "m0");
-}
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void*)p);
-}
-
-// Sequence position of key v of the list (segment boundaries b1 <= b2 <= b3;
-// segment 0 starts at s0, the shared map covers [b1, b2), segment 2 starts
-// at sa and segment 3 at sb).
-__device__ __forceinline__ int32_t list_seq(int32_t v, int32_t b1, int32_t b2, int32_t b3, int32_t s0,
-                                            int32_t sa, int32_t sb, const Spans& sp) {
-    if (v < b1) return s0 + v;
-    if (v < b2) return sp.map[v - b1];
-    if (v < b3) return sa + (v - b2);
-    return sb + (v - b3);
-}
 
 // PAD: the image span holds padding positions (a general shape).  A
 // separate instantiation, so that the square power-of-two path carries none

@@ -1,0 +1,508 @@
+// HilbertA attention backward, bf16: the gradients of the forward's masked
+// softmax attention (§3.2-§3.4, Appendix A), by the chain rule.  With
+// S = s Q K^T (masked), P = exp(S - LSE) the forward's probabilities, dO
+// the gradient of O:
+//   Dlt_i = dO_i . O_i,   dP = dO V^T,   dS = P (dP - Dlt),
+//   dV = P^T dO,          dK = s dS^T Q,   dQ = s dS K.
+// bf16 inputs and gradients, fp32 MFMA accumulation, P and dS rounded to
+// bf16 as MFMA operands.  Three launches:
+//   bwd_prep_kernel  Dlt and the LSE in log2 units, one per row;
+//   bwd_dq_kernel    the forward's query items and key lists: per stage
+//                    S^T = K Q^T and dP^T = V dO^T with the keys as A
+//                    operands, P and dS per lane (one query row per lane),
+//                    dQ^T += K^T dS^T with K read transposed;
+//   bwd_dkdv_kernel  key items: the list of a key block is the queries that
+//                    attend it, built as a query block's key list (the mask
+//                    is symmetric); S = Q K^T and dP = dO V^T with the
+//                    queries as A operands (one key row per lane), then
+//                    dV^T += dO^T P and dK^T += Q^T dS with Q and dO read
+//                    transposed.
+// No atomics: every gradient row is written once by the item that owns it,
+// so the results are deterministic.  Rows that attend every key (text and
+// shared rows) and keys every query attends are items of their own over the
+// whole sequence.  Each stage tensor is staged through LDS by direct loads
+// in the layout its reads need (fk for whole-row A operands, fv for the
+// transposing reads; Q, dO and K are read both ways and staged twice).
+// Their operands and accumulators take most of the register file, so each
+// SIMD runs one wavefront.
+#include "bf16_stage.hpp"
+
+namespace hilberta {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+// Dlt_i = dO_i . O_i in fp32 and lse2_i = LSE_i log2(e) (0 for a row that
+// attends nothing, whose probabilities are all masked anyway).  D/4 lanes
+// per row, four elements each.
+template <int D>
+__global__ void __launch_bounds__(256) bwd_prep_kernel(AttnArgs a, BwdArgs g) {
+    constexpr int LPR = D / 4;
+    constexpr int RPB = 256 / LPR;
+    const int sub = threadIdx.x % LPR;
+    const int64_t rowid = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
+    const int64_t rows = (int64_t)a.n_bh * a.n_tot;
+    const bool ok = rowid < rows;
+    const int64_t r = ok ? rowid : 0;
+    const int64_t bh = r / a.n_tot, n = r - bh * a.n_tot;
+    const int64_t b = bh / a.heads, hh = bh - b * a.heads;
+    const int64_t off = b * a.o_sb + hh * a.o_sh + n * a.o_sr + 4 * sub;
+    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+    const bf16x4 o4 = *reinterpret_cast<const bf16x4*>(reinterpret_cast<const __bf16*>(a.o) + off);
+    const bf16x4 d4 = *reinterpret_cast<const bf16x4*>(reinterpret_cast<const __bf16*>(g.dout) + off);
+    float t = (float)o4[0] * (float)d4[0] + (float)o4[1] * (float)d4[1] + (float)o4[2] * (float)d4[2] +
+              (float)o4[3] * (float)d4[3];
+#pragma unroll
+    for (int w = LPR / 2; w > 0; w >>= 1) t += __shfl_xor(t, w, LPR);
+    if (ok && sub == 0) {
+        g.delta[r] = t;
+        const float l = g.lse[r];
+        g.lse2[r] = l == -INFINITY ? 0.f : l * 1.4426950408889634f;
+    }
+}
+
+template <int D>
+__device__ __forceinline__ void store_grad(__bf16* row, const f32x16 acc[D / 32], float mul, int h) {
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            store4<__bf16>(row + 32 * dt + 8 * q + 4 * h, acc[dt][4 * q] * mul, acc[dt][4 * q + 1] * mul,
+                           acc[dt][4 * q + 2] * mul, acc[dt][4 * q + 3] * mul);
+}
+
+// Direct-load offsets of one lane for a stage tensor: lane l of load j fills
+// LDS chunk p = (w IPW + j) 64 + l, i.e. row p / CPR, stored chunk p % CPR,
+// which holds global chunk (p % CPR) ^ f(row).
+template <int D>
+struct LaneLoads {
+    int32_t srow[Geo<D>::IPW], colk[Geo<D>::IPW], colv[Geo<D>::IPW];
+    __device__ __forceinline__ void init(int wave, int lane) {
+#pragma unroll
+        for (int j = 0; j < Geo<D>::IPW; ++j) {
+            const int p = (wave * Geo<D>::IPW + j) * 64 + lane;
+            srow[j] = p / Geo<D>::CPR;
+            colk[j] = ((p % Geo<D>::CPR) ^ Geo<D>::fk(srow[j])) * 16;
+            colv[j] = ((p % Geo<D>::CPR) ^ Geo<D>::fv(srow[j])) * 16;
+        }
+    }
+};
+
+// ---------------------------------------------------------------------- dQ
+template <int D>
+struct SmemDq {
+    alignas(16) uint8_t k[2][Geo<D>::STAGEB];   // fk: A operand of S^T
+    alignas(16) uint8_t kt[2][Geo<D>::STAGEB];  // fv: transposed A operand of dQ^T
+    alignas(16) uint8_t v[2][Geo<D>::STAGEB];   // fk: A operand of dP^T
+    alignas(16) int32_t info[2][kBN];
+    Spans sp;
+    int32_t n_keep;
+    int32_t slow[2];
+};
+
+template <int D, bool PAD>
+__global__ void __launch_bounds__(kThreads, 1) bwd_dq_kernel(AttnArgs a, BwdArgs g) {
+    using G = Geo<D>;
+    __shared__ SmemDq<D> sm;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int h = lane >> 5;
+    const int ql = lane & 31;
+
+    const int item = remap_xcd(blockIdx.x, a.total_items);
+    const int32_t bh = item / a.items_per_bh;
+    const int32_t r = item - bh * a.items_per_bh;
+    const bool dense = r < a.dense_row_blocks;
+    const int32_t o = load_spans<kThreads>(a, sm.sp, tid);
+    const int32_t n_shared = a.sparse ? sm.sp.cum[sm.sp.n] : 0;
+    const int32_t row0 = dense ? r * kBlockMBf16 : (r - a.dense_row_blocks) * kBlockMBf16;
+    const ItemList L = item_list(a, dense, 0, row0, o, n_shared, sm.sp, sm.n_keep, wave, lane);
+    const int nblk = (L.total + kBN - 1) / kBN;
+    RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
+    if (!PAD) ri.pad = false;
+
+    const int32_t bb = bh / a.heads;
+    const int32_t hh = bh - bb * a.heads;
+    __bf16* dqrow = reinterpret_cast<__bf16*>(g.dq) + bb * a.q_sb + hh * a.q_sh + (int64_t)ri.qseq * a.q_sr;
+    if (PAD && !dense && !__syncthreads_or(ri.store && !ri.pad)) {
+        f32x16 zero[D / 32];
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) zero[dt] = f32x16{};
+        if (ri.store) store_grad<D>(dqrow, zero, 0.f, h);
+        return;
+    }
+    const int64_t qoff = bb * a.q_sb + hh * a.q_sh + (int64_t)ri.qseq * a.q_sr;
+    const int64_t ooff = bb * a.o_sb + hh * a.o_sh + (int64_t)ri.qseq * a.o_sr;
+    bf16x8 q[D / 16], dov[D / 16];
+#pragma unroll
+    for (int kc = 0; kc < D / 16; ++kc) {
+        q[kc] = *reinterpret_cast<const bf16x8*>(reinterpret_cast<const __bf16*>(a.q) + qoff + 16 * kc + 8 * h);
+        dov[kc] = *reinterpret_cast<const bf16x8*>(reinterpret_cast<const __bf16*>(g.dout) + ooff + 16 * kc + 8 * h);
+    }
+    const float lse2 = g.lse2[(int64_t)bh * a.n_tot + ri.qseq];
+    const float dlt = g.delta[(int64_t)bh * a.n_tot + ri.qseq];
+
+    const __bf16* kbase = reinterpret_cast<const __bf16*>(a.k) + bb * a.k_sb + hh * a.k_sh;
+    const __bf16* vbase = reinterpret_cast<const __bf16*>(a.v) + bb * a.v_sb + hh * a.v_sh;
+    const __amdgpu_buffer_rsrc_t krs = slice_rsrc(kbase, a.n_tot, a.k_sr, D, 2);
+    const __amdgpu_buffer_rsrc_t vrs = slice_rsrc(vbase, a.n_tot, a.v_sr, D, 2);
+    const int32_t krow_b = (int32_t)(a.k_sr * 2), vrow_b = (int32_t)(a.v_sr * 2);
+    LaneLoads<D> ll;
+    ll.init(wave, lane);
+    const uint32_t k0 = lds_addr(&sm.k[0][wave * G::IPW * 1024]);
+    const uint32_t kt0 = lds_addr(&sm.kt[0][wave * G::IPW * 1024]);
+    const uint32_t v0l = lds_addr(&sm.v[0][wave * G::IPW * 1024]);
+
+    auto stage_fast = [&](int32_t i) -> bool {
+        const int32_t v0 = i * kBN;
+        return L.total - v0 >= kBN && !(L.label_mask && v0 + kBN > L.b2);
+    };
+    auto load_stage = [&](int32_t i, int buf) {
+        const int32_t v0 = i * kBN;
+        const int32_t cnt = min(kBN, L.total - v0);
+        int32_t base = -1;
+        if (v0 + cnt <= L.b1) base = L.s0 + v0;
+        else if (v0 >= L.b2 && v0 + cnt <= L.b3) base = L.sa + (v0 - L.b2);
+        else if (v0 >= L.b3) base = L.sb + (v0 - L.b3);
+        if (PAD) {
+            const int32_t v = v0 + lane;
+            const int32_t seq = v >= L.total ? 0 : base >= 0 ? base + lane
+                                                            : list_seq(v, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
+            const int32_t inf = entry_info<true>(a, L, v, seq, o, sm.sp);
+            const bool none = __builtin_amdgcn_ballot_w64(inf != kKeyInvalid) == 0;
+            if (wave == 0) {
+                sm.info[buf][lane] = inf;
+                const bool slow = __builtin_amdgcn_ballot_w64(inf != kKeyAll) != 0;
+                if (lane == 0) sm.slow[buf] = none ? 2 : slow ? 1 : 0;
+            }
+            if (none) return;
+        }
+        const uint32_t off = buf * G::STAGEB;
+#pragma unroll
+        for (int j = 0; j < G::IPW; ++j) {
+            int32_t key;
+            if (base >= 0 && cnt == kBN) {
+                key = base + ll.srow[j];
+            } else {
+                // absent rows of a ragged stage re-read a present row (masked)
+                const int32_t rr = min(ll.srow[j], cnt - 1);
+                key = base >= 0 ? base + rr : list_seq(v0 + rr, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
+            }
+            dma16(krs, k0 + off + j * 1024, key * krow_b + ll.colk[j]);
+            dma16(krs, kt0 + off + j * 1024, key * krow_b + ll.colv[j]);
+            dma16(vrs, v0l + off + j * 1024, key * vrow_b + ll.colk[j]);
+        }
+        if (!PAD && !stage_fast(i) && tid < kBN) {
+            const int32_t v = v0 + tid;
+            const int32_t seq = v >= L.total ? 0 : list_seq(v, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
+            sm.info[buf][tid] = entry_info<false>(a, L, v, seq, o, sm.sp);
+        }
+    };
+
+    const int ka = row_base<D>(lane);
+    const int va = tr_base<D>(lane);
+    f32x16 acc[D / 32];
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) acc[dt] = f32x16{};
+    const float c = a.scale_log2;
+
+    wait_vmcnt<0>();
+    load_stage(0, 0);
+    wait_vmcnt<0>();
+    __syncthreads();
+    for (int32_t i = 0; i < nblk; ++i) {
+        const int buf = i & 1;
+        if (i + 1 < nblk) load_stage(i + 1, buf ^ 1);
+        if (!PAD || sm.slow[buf] != 2) {
+            const uint8_t* kb_ = sm.k[buf];
+            const uint8_t* vb_ = sm.v[buf];
+            // S^T = K Q^T and dP^T = V dO^T: register e of s[kt], dp[kt]
+            // holds key 32 kt + 8 (e/4) + 4 h + e%4 against this lane's row
+            f32x16 s[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+            for (int kc = 0; kc < D / 16; ++kc)
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt) {
+                    const int ad = (ka ^ (32 * kc)) + kt * 32 * G::ROWB;
+                    s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(kb_ + ad),
+                                                                    q[kc], s[kt], 0, 0, 0);
+                    dp[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(vb_ + ad),
+                                                                     dov[kc], dp[kt], 0, 0, 0);
+                }
+            if (PAD ? sm.slow[buf] != 0 : !stage_fast(i)) {
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        const int32_t inf = sm.info[buf][32 * kt + 8 * (e >> 2) + 4 * h + (e & 3)];
+                        s[kt][e] = (inf == kKeyAll || inf == ri.label) ? s[kt][e] : -INFINITY;
+                    }
+            }
+            // dS = P (dP - Dlt), rounded to bf16 in the key order of the
+            // transposed K operand: chunk cc, register j = key 16 cc + 8 (j/4)
+            // + 4 h + j%4
+            bf16x8 ds[4];
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int e = 8 * (cc & 1) + j;
+                    const float pe = __builtin_amdgcn_exp2f(fmaf(s[cc >> 1][e], c, -lse2));
+                    ds[cc][j] = (__bf16)(pe * (dp[cc >> 1][e] - dlt));
+                }
+            const uint8_t* ktb = sm.kt[buf];
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+                for (int dt = 0; dt < D / 32; ++dt)
+                    acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(ktb, va, cc, dt), ds[cc], acc[dt],
+                                                                      0, 0, 0);
+        }
+        wait_vmcnt<0>();
+        __syncthreads();
+    }
+    if (!ri.store) return;
+    store_grad<D>(dqrow, acc, ri.pad ? 0.f : a.scale_log2 * 0.69314718055994530942f, h);
+}
+
+// -------------------------------------------------------------------- dK dV
+template <int D>
+struct SmemDkdv {
+    alignas(16) uint8_t q[2][Geo<D>::STAGEB];   // fk: A operand of S
+    alignas(16) uint8_t qt[2][Geo<D>::STAGEB];  // fv: transposed A operand of dK^T
+    alignas(16) uint8_t d[2][Geo<D>::STAGEB];   // fk: dO, A operand of dP
+    alignas(16) uint8_t dt[2][Geo<D>::STAGEB];  // fv: dO, transposed A operand of dV^T
+    alignas(16) float lse2[2][kBN];
+    alignas(16) float dlt[2][kBN];
+    alignas(16) int32_t info[2][kBN];
+    Spans sp;
+    int32_t n_keep;
+    int32_t slow[2];
+};
+
+template <int D, bool PAD>
+__global__ void __launch_bounds__(kThreads, 1) bwd_dkdv_kernel(AttnArgs a, BwdArgs g) {
+    using G = Geo<D>;
+    __shared__ SmemDkdv<D> sm;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int h = lane >> 5;
+    const int ql = lane & 31;
+
+    const int item = remap_xcd(blockIdx.x, a.total_items);
+    const int32_t bh = item / a.items_per_bh;
+    const int32_t r = item - bh * a.items_per_bh;
+    const bool dense = r < a.dense_row_blocks;
+    const int32_t o = load_spans<kThreads>(a, sm.sp, tid);
+    const int32_t n_shared = a.sparse ? sm.sp.cum[sm.sp.n] : 0;
+    const int32_t row0 = dense ? r * kBlockMBf16 : (r - a.dense_row_blocks) * kBlockMBf16;
+    const ItemList L = item_list(a, dense, 0, row0, o, n_shared, sm.sp, sm.n_keep, wave, lane);
+    const int nblk = (L.total + kBN - 1) / kBN;
+    // this lane's key row (the item's rows are keys here)
+    RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
+    if (!PAD) ri.pad = false;
+
+    const int32_t bb = bh / a.heads;
+    const int32_t hh = bh - bb * a.heads;
+    __bf16* dkrow = reinterpret_cast<__bf16*>(g.dk) + bb * a.k_sb + hh * a.k_sh + (int64_t)ri.qseq * a.k_sr;
+    __bf16* dvrow = reinterpret_cast<__bf16*>(g.dv) + bb * a.v_sb + hh * a.v_sh + (int64_t)ri.qseq * a.v_sr;
+    if (PAD && !dense && !__syncthreads_or(ri.store && !ri.pad)) {
+        f32x16 zero[D / 32];
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) zero[dt] = f32x16{};
+        if (ri.store) {
+            store_grad<D>(dkrow, zero, 0.f, h);
+            store_grad<D>(dvrow, zero, 0.f, h);
+        }
+        return;
+    }
+    const int64_t koff = bb * a.k_sb + hh * a.k_sh + (int64_t)ri.qseq * a.k_sr;
+    const int64_t voff = bb * a.v_sb + hh * a.v_sh + (int64_t)ri.qseq * a.v_sr;
+    bf16x8 kr[D / 16], vr[D / 16];
+#pragma unroll
+    for (int kc = 0; kc < D / 16; ++kc) {
+        kr[kc] = *reinterpret_cast<const bf16x8*>(reinterpret_cast<const __bf16*>(a.k) + koff + 16 * kc + 8 * h);
+        vr[kc] = *reinterpret_cast<const bf16x8*>(reinterpret_cast<const __bf16*>(a.v) + voff + 16 * kc + 8 * h);
+    }
+
+    const __bf16* qbase = reinterpret_cast<const __bf16*>(a.q) + bb * a.q_sb + hh * a.q_sh;
+    const __bf16* dbase = reinterpret_cast<const __bf16*>(g.dout) + bb * a.o_sb + hh * a.o_sh;
+    const __amdgpu_buffer_rsrc_t qrs = slice_rsrc(qbase, a.n_tot, a.q_sr, D, 2);
+    const __amdgpu_buffer_rsrc_t drs = slice_rsrc(dbase, a.n_tot, a.o_sr, D, 2);
+    const int32_t qrow_b = (int32_t)(a.q_sr * 2), drow_b = (int32_t)(a.o_sr * 2);
+    const float* lse2_bh = g.lse2 + (int64_t)bh * a.n_tot;
+    const float* dlt_bh = g.delta + (int64_t)bh * a.n_tot;
+    LaneLoads<D> ll;
+    ll.init(wave, lane);
+    const uint32_t q0 = lds_addr(&sm.q[0][wave * G::IPW * 1024]);
+    const uint32_t qt0 = lds_addr(&sm.qt[0][wave * G::IPW * 1024]);
+    const uint32_t d0 = lds_addr(&sm.d[0][wave * G::IPW * 1024]);
+    const uint32_t dt0 = lds_addr(&sm.dt[0][wave * G::IPW * 1024]);
+
+    // per-query LSE and Dlt of the stage being loaded: read into registers
+    // by wavefront 0 (lane = list entry) and written to LDS before the
+    // barrier that publishes the stage
+    float nl = 0.f, nd = 0.f;
+    auto stage_fast = [&](int32_t i) -> bool {
+        const int32_t v0 = i * kBN;
+        return L.total - v0 >= kBN && !(L.label_mask && v0 + kBN > L.b2);
+    };
+    auto load_stage = [&](int32_t i, int buf) {
+        const int32_t v0 = i * kBN;
+        const int32_t cnt = min(kBN, L.total - v0);
+        int32_t base = -1;
+        if (v0 + cnt <= L.b1) base = L.s0 + v0;
+        else if (v0 >= L.b2 && v0 + cnt <= L.b3) base = L.sa + (v0 - L.b2);
+        else if (v0 >= L.b3) base = L.sb + (v0 - L.b3);
+        const int32_t v = v0 + lane;
+        const int32_t seq = v >= L.total ? 0 : base >= 0 ? base + lane
+                                                        : list_seq(v, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
+        if (PAD) {
+            const int32_t inf = entry_info<true>(a, L, v, seq, o, sm.sp);
+            const bool none = __builtin_amdgcn_ballot_w64(inf != kKeyInvalid) == 0;
+            if (wave == 0) {
+                sm.info[buf][lane] = inf;
+                const bool slow = __builtin_amdgcn_ballot_w64(inf != kKeyAll) != 0;
+                if (lane == 0) sm.slow[buf] = none ? 2 : slow ? 1 : 0;
+            }
+            if (none) return;
+        }
+        if (wave == 0) {
+            nl = lse2_bh[seq];
+            nd = dlt_bh[seq];
+        }
+        const uint32_t off = buf * G::STAGEB;
+#pragma unroll
+        for (int j = 0; j < G::IPW; ++j) {
+            int32_t qs;
+            if (base >= 0 && cnt == kBN) {
+                qs = base + ll.srow[j];
+            } else {
+                const int32_t rr = min(ll.srow[j], cnt - 1);
+                qs = base >= 0 ? base + rr : list_seq(v0 + rr, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
+            }
+            dma16(qrs, q0 + off + j * 1024, qs * qrow_b + ll.colk[j]);
+            dma16(qrs, qt0 + off + j * 1024, qs * qrow_b + ll.colv[j]);
+            dma16(drs, d0 + off + j * 1024, qs * drow_b + ll.colk[j]);
+            dma16(drs, dt0 + off + j * 1024, qs * drow_b + ll.colv[j]);
+        }
+        if (!PAD && !stage_fast(i) && tid < kBN) sm.info[buf][tid] = entry_info<false>(a, L, v, seq, o, sm.sp);
+    };
+
+    const int ka = row_base<D>(lane);
+    const int va = tr_base<D>(lane);
+    f32x16 acck[D / 32], accv[D / 32];
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) {
+        acck[dt] = f32x16{};
+        accv[dt] = f32x16{};
+    }
+    const float c = a.scale_log2;
+
+    wait_vmcnt<0>();
+    load_stage(0, 0);
+    wait_vmcnt<0>();
+    if (wave == 0) {
+        sm.lse2[0][lane] = nl;
+        sm.dlt[0][lane] = nd;
+    }
+    __syncthreads();
+    for (int32_t i = 0; i < nblk; ++i) {
+        const int buf = i & 1;
+        if (i + 1 < nblk) load_stage(i + 1, buf ^ 1);
+        if (!PAD || sm.slow[buf] != 2) {
+            const uint8_t* qb = sm.q[buf];
+            const uint8_t* db = sm.d[buf];
+            // S = Q K^T and dP = dO V^T: register e of s[kt], dp[kt] holds
+            // query 32 kt + 8 (e/4) + 4 h + e%4 against this lane's key
+            f32x16 s[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+            for (int kc = 0; kc < D / 16; ++kc)
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt) {
+                    const int ad = (ka ^ (32 * kc)) + kt * 32 * G::ROWB;
+                    s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(qb + ad),
+                                                                    kr[kc], s[kt], 0, 0, 0);
+                    dp[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(db + ad),
+                                                                     vr[kc], dp[kt], 0, 0, 0);
+                }
+            if (PAD ? sm.slow[buf] != 0 : !stage_fast(i)) {
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        const int32_t inf = sm.info[buf][32 * kt + 8 * (e >> 2) + 4 * h + (e & 3)];
+                        s[kt][e] = (inf == kKeyAll || inf == ri.label) ? s[kt][e] : -INFINITY;
+                    }
+            }
+            // P and dS per query, in the order of the transposed operands
+            bf16x8 pb[4], ds[4];
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+                for (int j4 = 0; j4 < 2; ++j4) {
+                    const int kt = cc >> 1, g4 = 2 * (cc & 1) + j4;
+                    const int q0i = 32 * kt + 8 * g4 + 4 * h;
+                    const f4 l4 = *reinterpret_cast<const f4*>(&sm.lse2[buf][q0i]);
+                    const f4 d4 = *reinterpret_cast<const f4*>(&sm.dlt[buf][q0i]);
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        const int e = 4 * g4 + t;
+                        const float pe = __builtin_amdgcn_exp2f(fmaf(s[kt][e], c, -l4[t]));
+                        pb[cc][4 * j4 + t] = (__bf16)pe;
+                        ds[cc][4 * j4 + t] = (__bf16)(pe * (dp[kt][e] - d4[t]));
+                    }
+                }
+            const uint8_t* dtb = sm.dt[buf];
+            const uint8_t* qtb = sm.qt[buf];
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+                for (int dt = 0; dt < D / 32; ++dt) {
+                    accv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(dtb, va, cc, dt), pb[cc],
+                                                                       accv[dt], 0, 0, 0);
+                    acck[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(qtb, va, cc, dt), ds[cc],
+                                                                       acck[dt], 0, 0, 0);
+                }
+        }
+        wait_vmcnt<0>();
+        if (wave == 0 && i + 1 < nblk) {
+            sm.lse2[buf ^ 1][lane] = nl;
+            sm.dlt[buf ^ 1][lane] = nd;
+        }
+        __syncthreads();
+    }
+    if (!ri.store) return;
+    store_grad<D>(dkrow, acck, ri.pad ? 0.f : a.scale_log2 * 0.69314718055994530942f, h);
+    store_grad<D>(dvrow, accv, ri.pad ? 0.f : 1.f, h);
+}
+
+template <int D>
+hipError_t launch_bwd_t(const AttnArgs& a, const BwdArgs& g, hipStream_t s) {
+    const int64_t rows = (int64_t)a.n_bh * a.n_tot;
+    constexpr int64_t rpb = 256 / (D / 4);
+    const int64_t pblocks = (rows + rpb - 1) / rpb;
+    if (pblocks > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((bwd_prep_kernel<D>), dim3((unsigned)pblocks), dim3(256), 0, s, a, g);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (a.padded) {
+        hipLaunchKernelGGL((bwd_dq_kernel<D, true>), dim3(a.total_items), dim3(kThreads), 0, s, a, g);
+        hipLaunchKernelGGL((bwd_dkdv_kernel<D, true>), dim3(a.total_items), dim3(kThreads), 0, s, a, g);
+    } else {
+        hipLaunchKernelGGL((bwd_dq_kernel<D, false>), dim3(a.total_items), dim3(kThreads), 0, s, a, g);
+        hipLaunchKernelGGL((bwd_dkdv_kernel<D, false>), dim3(a.total_items), dim3(kThreads), 0, s, a, g);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attn_bwd(const AttnArgs& a, const BwdArgs& g, int head_dim, hipStream_t s) {
+    if (a.total_items == 0) return hipSuccess;
+    return head_dim == 128 ? launch_bwd_t<128>(a, g, s) : launch_bwd_t<64>(a, g, s);
+}
+
+}  // namespace hilberta

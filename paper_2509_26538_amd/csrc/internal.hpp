@@ -82,6 +82,20 @@ hipError_t launch_attn(const AttnArgs& a, int dtype, int head_dim, hipStream_t s
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& m, int dtype, int head_dim, hipStream_t s);
 
+// Backward (attn_bwd.hip): the forward's AttnArgs (Q, K, V, O and their
+// strides, the item decomposition without split key passes) plus these.
+// dO shares O's strides, dQ Q's, dK K's and dV V's.
+struct BwdArgs {
+    const void* dout;
+    const float* lse;   // natural-log LSE of the forward, [B*H*N_tot]
+    void* dq;
+    void* dk;
+    void* dv;
+    float* delta;       // workspace: dO . O per row, [B*H*N_tot]
+    float* lse2;        // workspace: LSE in log2 units (0 for empty rows)
+};
+hipError_t launch_attn_bwd(const AttnArgs& a, const BwdArgs& g, int head_dim, hipStream_t s);
+
 // ----------------------------------------------------- permutation, schedule
 // perm[d] for the side x side curve positions: the raster index of the
 // grid_h x grid_w grid's cell at d, or -1 for a padding slot

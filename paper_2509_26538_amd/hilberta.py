@@ -28,7 +28,8 @@ EXPORTS = [
     "hilberta_build_perm_layout", "hilberta_permute",
     "hilberta_unpermute", "hilberta_schedule_words", "hilberta_schedule",
     "hilberta_attn_workspace_bytes", "hilberta_attn_fwd", "dense_attn_workspace_bytes",
-    "dense_attn_fwd",
+    "dense_attn_fwd", "hilberta_attn_bwd_workspace_bytes", "hilberta_attn_bwd",
+    "dense_attn_bwd_workspace_bytes", "dense_attn_bwd",
 ]
 
 
@@ -79,6 +80,12 @@ def load(path=LIB_PATH):
         "dense_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _I64, _I64, _I64, _I64,
                                           _STR4, _STR4, _STR4, _STR4, ctypes.c_int,
                                           ctypes.c_float, _P, _I64, _P]),
+        "hilberta_attn_bwd_workspace_bytes": (ctypes.c_int, [_CFGP, _I64, _I64, _I64, ctypes.c_int, _I64P]),
+        "hilberta_attn_bwd": (ctypes.c_int, [_CFGP, _P] + [_P] * 9 + [_I64, _I64, _I64] +
+                              [_STR4] * 4 + [ctypes.c_int, ctypes.c_float, _P, _I64, _P]),
+        "dense_attn_bwd_workspace_bytes": (ctypes.c_int, [_I64, _I64, _I64, _I64, ctypes.c_int, _I64P]),
+        "dense_attn_bwd": (ctypes.c_int, [_P] * 9 + [_I64, _I64, _I64, _I64] +
+                           [_STR4] * 4 + [ctypes.c_int, ctypes.c_float, _P, _I64, _P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -259,3 +266,52 @@ def dense_attn_fwd(q, k, v, o, lse=None, scale=None, workspace=None, stream=None
     _check(load().dense_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), b, h, n, d,
                                  _strides(q), _strides(k), _strides(v), _strides(o), _dtype(q),
                                  scale, wp, wb, _stream(stream)))
+
+
+def hilberta_attn_bwd_workspace_bytes(cfg, batch, heads, head_dim, dtype):
+    out = ctypes.c_int64(0)
+    _check(load().hilberta_attn_bwd_workspace_bytes(ctypes.byref(cfg), batch, heads, head_dim, dtype,
+                                                    ctypes.byref(out)))
+    return out.value
+
+
+def dense_attn_bwd_workspace_bytes(batch, heads, n, head_dim, dtype):
+    out = ctypes.c_int64(0)
+    _check(load().dense_attn_bwd_workspace_bytes(batch, heads, n, head_dim, dtype, ctypes.byref(out)))
+    return out.value
+
+
+def _bwd_checks(q, k, v, o, dout, lse, dq, dk, dv):
+    _same_dtype(q, k, v, o, lse)
+    if lse is None:
+        raise HilbertaError(HILBERTA_EINVAL, "the backward needs the forward's lse")
+    for a, b, name in ((dout, o, "dout"), (dq, q, "dq"), (dk, k, "dk"), (dv, v, "dv")):
+        if a.dtype != b.dtype or a.shape != b.shape or a.stride() != b.stride():
+            raise HilbertaError(HILBERTA_EINVAL, "%s must match the shape, dtype and strides of its tensor"
+                                % name)
+
+
+def hilberta_attn_bwd(cfg, sched, q, k, v, o, dout, lse, dq, dk, dv, workspace, scale=None, stream=None):
+    """Gradients dq, dk, dv of the HilbertA attention for upstream gradient
+    dout, from the forward's q, k, v, o and lse [B, H, N_tot]."""
+    b, h, n, d = q.shape
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    _bwd_checks(q, k, v, o, dout, lse, dq, dk, dv)
+    wp, wb = _ws(workspace)
+    _check(load().hilberta_attn_bwd(ctypes.byref(cfg), _ptr(sched), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
+                                    _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv), b, h, d,
+                                    _strides(q), _strides(k), _strides(v), _strides(o), _dtype(q), scale,
+                                    wp, wb, _stream(stream)))
+
+
+def dense_attn_bwd(q, k, v, o, dout, lse, dq, dk, dv, workspace, scale=None, stream=None):
+    """Gradients of full softmax attention (the dense baseline)."""
+    b, h, n, d = q.shape
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    _bwd_checks(q, k, v, o, dout, lse, dq, dk, dv)
+    wp, wb = _ws(workspace)
+    _check(load().dense_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lse), _ptr(dq),
+                                 _ptr(dk), _ptr(dv), b, h, n, d, _strides(q), _strides(k), _strides(v),
+                                 _strides(o), _dtype(q), scale, wp, wb, _stream(stream)))

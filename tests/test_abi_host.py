@@ -193,3 +193,28 @@ def test_permute_errors(lib):
 @pytest.mark.parametrize("h,w", [(1, 1), (2, 2), (3, 5), (96, 96), (128, 128), (129, 3), (1, 32768)])
 def test_image_span_matches_the_oracle(h, w):
     assert hb.image_span(h, w) == osched.Layout(h, w, 0, 1, 0).n_img
+
+
+def _bwd(lib, cfg=None, dtype=hb.HILBERTA_BF16, lse=FAKE, ws=FAKE, wsb=1 << 30, d=64, q=FAKE):
+    cfg = cfg or hb.make_config(16, 0, 64, 32, 4)
+    n = cfg.n_txt + hb.image_span(cfg.grid_h, cfg.grid_w)
+    s = strides(1, 2, n, d)
+    return lib.hilberta_attn_bwd(ctypes.byref(cfg), FAKE, q, FAKE, FAKE, FAKE, FAKE, lse, FAKE, FAKE, FAKE,
+                                 1, 2, d, s, s, s, s, dtype, 0.125, ws, wsb, None)
+
+
+def test_backward_argument_errors(lib):
+    # every call fails validation before any launch
+    assert _bwd(lib, dtype=hb.HILBERTA_F32) == hb.HILBERTA_EUNSUPPORTED
+    assert "bf16" in hb.last_error()
+    assert _bwd(lib, lse=None) == hb.HILBERTA_EINVAL
+    assert _bwd(lib, ws=None, wsb=0) == hb.HILBERTA_EINVAL
+    assert _bwd(lib, wsb=100) == hb.HILBERTA_ECAPACITY
+    assert _bwd(lib, d=96) == hb.HILBERTA_EUNSUPPORTED
+    assert _bwd(lib, q=None) == hb.HILBERTA_EINVAL
+    assert _bwd(lib, cfg=hb.hilberta_config(6, 6, 0, 7, 2, 0, 0)) == hb.HILBERTA_EUNSUPPORTED
+    assert hb.hilberta_attn_bwd_workspace_bytes(hb.make_config(16, 0, 64, 32, 4), 1, 2, 64,
+                                                hb.HILBERTA_BF16) == 2 * 256 * 8
+    assert hb.dense_attn_bwd_workspace_bytes(2, 3, 100, 128, hb.HILBERTA_BF16) == 6 * 100 * 8
+    with pytest.raises(hb.HilbertaError):
+        hb.dense_attn_bwd_workspace_bytes(2, 3, 100, 128, hb.HILBERTA_F32)

@@ -1,0 +1,170 @@
+"""GPU parity of hilberta_attn_bwd and dense_attn_bwd (bf16) against the
+float64 oracle's gradients on the same bf16-rounded Q, K, V and dO.
+
+The GPU backward reads the forward's O and LSE from the GPU forward (its
+inputs, as in training); the oracle differentiates its own float64
+attention.  Bounds (see BWD_MAX_REL below) are relative to each gradient
+tensor's largest magnitude.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import gradients, schedule
+from oracle.schedule import Layout
+from paper_2509_26538_amd import hilberta as hb
+from paper_2509_26538_amd import synth
+
+from attn_util import make_schedule, workspace
+
+pytestmark = pytest.mark.gpu
+
+# bf16 rounding budget.  One bf16 rounding is at most u = 2^-9 relative.  Each
+# gradient element is a sum of products of one rounded operand (P for dV, dS
+# for dQ and dK) with exact bf16 inputs, accumulated in fp32, then rounded
+# once more on output (at most u of the tensor's largest magnitude); the
+# forward's bf16 O enters dS through Dlt = dO . O.  The operand roundings
+# add up to u of the sum of the terms' magnitudes, which cancellation can
+# make larger than the result: the bound allows 4 u of the tensor's largest
+# magnitude in total, max|err| <= 2^-7 max|ref|, and a mean error of u/4,
+# mean|err| <= 2^-11 max|ref|.  Measured on the layouts below: max 1.3-2.5 u,
+# mean 0.05-0.12 u.
+BWD_MAX_REL = 2.0 ** -7
+BWD_MEAN_REL = 2.0 ** -11
+
+
+def inputs(n_tot, batch, heads, d, seed):
+    q, k, v = synth.qkv(batch, heads, n_tot, d, "bf16", seed=seed)
+    g = torch.Generator(device="cpu").manual_seed(seed + 1000)
+    do = torch.randn(batch, heads, n_tot, d, generator=g).to(torch.bfloat16)
+    return q, k, v, do
+
+
+def run_sparse(layout, layer, q, k, v, do, dev):
+    cfg, sched = make_schedule(layout, layer, dev)
+    qd, kd, vd, dod = (t.to(dev) for t in (q, k, v, do))
+    b, h, n, d = q.shape
+    o = torch.empty_like(qd)
+    lse = torch.empty(b, h, n, dtype=torch.float32, device=dev)
+    ws = workspace(hb.hilberta_attn_workspace_bytes(cfg, b, h, d, hb.HILBERTA_BF16), dev)
+    hb.hilberta_attn_fwd(cfg, sched, qd, kd, vd, o, lse, workspace=ws)
+    grads = [torch.full_like(qd, float("nan")) for _ in range(3)]
+    bws = torch.empty(hb.hilberta_attn_bwd_workspace_bytes(cfg, b, h, d, hb.HILBERTA_BF16),
+                      dtype=torch.uint8, device=dev)
+    hb.hilberta_attn_bwd(cfg, sched, qd, kd, vd, o, dod, lse, *grads, bws)
+    torch.cuda.synchronize()
+    return [g.cpu().to(torch.float64).numpy() for g in grads]
+
+
+def run_dense(q, k, v, do, dev):
+    qd, kd, vd, dod = (t.to(dev) for t in (q, k, v, do))
+    b, h, n, d = q.shape
+    o = torch.empty_like(qd)
+    lse = torch.empty(b, h, n, dtype=torch.float32, device=dev)
+    hb.dense_attn_fwd(qd, kd, vd, o, lse)
+    grads = [torch.full_like(qd, float("nan")) for _ in range(3)]
+    bws = torch.empty(hb.dense_attn_bwd_workspace_bytes(b, h, n, d, hb.HILBERTA_BF16), dtype=torch.uint8,
+                      device=dev)
+    hb.dense_attn_bwd(qd, kd, vd, o, dod, lse, *grads, bws)
+    torch.cuda.synchronize()
+    return [g.cpu().to(torch.float64).numpy() for g in grads]
+
+
+def oracle(q, k, v, do, mask_fn):
+    a = [t.to(torch.float64).numpy() for t in (q, k, v, do)]
+    return gradients.masked_attention_grads(*a, mask_fn)
+
+
+def assert_grads(got, ref, what):
+    for name, g, r in zip(("dq", "dk", "dv"), got, ref):
+        assert np.all(np.isfinite(g)), "%s %s: non-finite (unwritten rows?)" % (what, name)
+        scale = np.abs(r).max()
+        err = np.abs(g - r)
+        assert err.max() <= BWD_MAX_REL * scale, "%s %s: max err %.3g, scale %.3g" % (
+            what, name, err.max(), scale)
+        assert err.mean() <= BWD_MEAN_REL * scale, "%s %s: mean err %.3g, scale %.3g" % (
+            what, name, err.mean(), scale)
+
+
+LAYOUTS = [
+    Layout(16, 16, 0, 64, 32, 4, 4),
+    Layout(16, 16, 77, 64, 40, 4, 4),
+    Layout(32, 32, 13, 256, 96, 8, 8),
+    Layout(32, 32, 130, 32, 24, 7, 5),     # tiles shorter than a block: label masks
+    Layout(16, 16, 5, 256, 16, 0, 0),      # one tile
+    Layout(8, 8, 3, 16, 5, 3, 2),
+    Layout(16, 16, 7, 48, 12, 4, 4, moved=True),
+    Layout(12, 16, 3, 64, 16, 4, 4),       # general shape: padding
+    Layout(33, 20, 130, 512, 128, 6, 4),   # general shape, ragged
+]
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_sparse_backward(gpu, layout, head_dim):
+    q, k, v, do = inputs(layout.n_tot, 1, 2, head_dim, seed=layout.n_tot + head_dim)
+    for layer in (0, 1, 3):
+        got = run_sparse(layout, layer, q, k, v, do, gpu)
+        ref = oracle(q, k, v, do, lambda rows: schedule.mask_rows(layout, layer, rows))
+        assert_grads(got, ref, "layer %d" % layer)
+        if layout.padded:
+            pad = layout.n_txt + np.nonzero(~schedule.valid_hilbert(layout))[0]
+            for g in got:
+                assert np.all(g[:, :, pad] == 0)
+
+
+@pytest.mark.parametrize("n,head_dim", [(200, 64), (333, 128), (64, 128)])
+def test_dense_backward(gpu, n, head_dim):
+    q, k, v, do = inputs(n, 2, 2, head_dim, seed=n)
+    got = run_dense(q, k, v, do, gpu)
+    ref = oracle(q, k, v, do, lambda rows: np.ones((len(rows), n), dtype=bool))
+    assert_grads(got, ref, "dense")
+
+
+def test_backward_is_deterministic(gpu):
+    layout = Layout(32, 32, 13, 256, 96, 8, 8)
+    q, k, v, do = inputs(layout.n_tot, 1, 2, 128, seed=1)
+    a = run_sparse(layout, 1, q, k, v, do, gpu)
+    b = run_sparse(layout, 1, q, k, v, do, gpu)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+def sampled_keys(layout, layer, rng, n_tile_keys, n_global):
+    """Key rows to check: non-global image keys (both sides of a tile
+    boundary and random ones), and a few text and shared keys."""
+    is_global, lab = schedule.token_classes(layout, layer)
+    img = np.arange(layout.n_txt, layout.n_tot)
+    cand = img[~is_global[img]]
+    if layout.padded:
+        cand = cand[schedule.token_valid(layout)[cand]]
+    edges = cand[np.nonzero(lab[cand] != np.roll(lab[cand], 1))[0]]
+    keys = set(int(e) for e in edges[:2]) | set(int(e) - 1 for e in edges[:2] if e - 1 in set(cand.tolist()))
+    keys |= set(int(x) for x in rng.choice(cand, n_tile_keys, replace=False))
+    glob = np.nonzero(is_global)[0]
+    keys |= set(int(x) for x in rng.choice(glob, n_global, replace=False)) if n_global else set()
+    return np.array(sorted(keys), dtype=np.int64)
+
+
+@pytest.mark.parametrize("name,n_global", [("flux-64", 2), ("flux-128", 0)])
+def test_fullsize_sampled_rows(gpu, name, n_global):
+    # the benchmark's shapes (bf16, 24 heads, D 128): every gradient element
+    # finite, and sampled rows of three heads against the oracle
+    w = synth.WORKLOADS[name]
+    layout = Layout(w.grid, w.cols, w.n_txt, w.tile, w.delta, w.shared, w.shared)
+    layer = 1
+    q, k, v, do = inputs(layout.n_tot, 1, w.heads, w.head_dim, seed=w.seed)
+    got = run_sparse(layout, layer, q, k, v, do, gpu)
+    for g in got:
+        assert np.all(np.isfinite(g))
+    heads = [0, 13, 23]
+    rng = np.random.default_rng(3)
+    from test_gpu_fullsize import sample_rows
+    q_rows = sample_rows(layout, layer, n_random=12, seed=5)
+    k_rows = sampled_keys(layout, layer, rng, 4, n_global)
+    a = [t[:, heads].to(torch.float64).numpy() for t in (q, k, v, do)]
+    ref = gradients.masked_attention_grads_rows(*a, lambda rows: schedule.mask_rows(layout, layer, rows),
+                                                q_rows, k_rows)
+    sub = [got[0][:, heads][:, :, q_rows], got[1][:, heads][:, :, k_rows], got[2][:, heads][:, :, k_rows]]
+    assert_grads(sub, list(ref), "%s rows" % name)

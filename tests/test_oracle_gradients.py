@@ -105,3 +105,17 @@ def test_padding_gets_zero_gradient_and_leaks_nothing():
     g2 = gradients.masked_attention_grads(q2, k2, v2, do2, f)
     for a, b in zip(g1, g2):
         assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_sampled_rows_match_the_full_gradients(layout):
+    q, k, v, do = _inputs(layout.n_tot, 8, 4)
+    f = lambda rows: schedule.mask_rows(layout, 2, rows)  # noqa: E731
+    full = gradients.masked_attention_grads(q, k, v, do, f)
+    rng = np.random.default_rng(0)
+    qr = rng.choice(layout.n_tot, 7, replace=False)
+    kr = rng.choice(layout.n_tot, 5, replace=False)
+    dq, dk, dv = gradients.masked_attention_grads_rows(q, k, v, do, f, qr, kr, block=9)
+    np.testing.assert_allclose(dq, full[0][:, :, qr], rtol=0, atol=1e-13)
+    np.testing.assert_allclose(dk, full[1][:, :, kr], rtol=0, atol=1e-13)
+    np.testing.assert_allclose(dv, full[2][:, :, kr], rtol=0, atol=1e-13)
