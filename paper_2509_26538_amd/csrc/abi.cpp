@@ -338,8 +338,15 @@ int run_attention(bool sparse, const hilberta_config* cfg, const int32_t* sched,
     return hip_status(hilberta::launch_merge(m, dtype, (int)head_dim, s), "merge launch");
 }
 
-// Workspace of the backward: dO . O and the base-2 LSE per row.
-int64_t bwd_ws_bytes(int64_t bh, int64_t n_tot) { return bh * n_tot * 2 * 4; }
+// Workspace of the backward: dO . O and the base-2 LSE per row, then the
+// chunk partials of the split dense rows (two D-vectors per row and chunk,
+// reused by the dQ and the dK/dV passes).
+int64_t bwd_rows_bytes(int64_t bh, int64_t n_tot) { return round_up(bh * n_tot * 2, 4) * 4; }
+
+int64_t bwd_ws_bytes(const Plan& p, int64_t bh, int64_t n_tot, int64_t head_dim) {
+    const int64_t part = p.n_chunks > 1 ? bh * p.n_chunks * p.n_dense_rows * 2 * head_dim * 4 : 0;
+    return bwd_rows_bytes(bh, n_tot) + part;
+}
 
 int run_attention_bwd(bool sparse, const hilberta_config* cfg, const int32_t* sched, const void* q,
                       const void* k, const void* v, const void* o, const void* dout, const float* lse,
@@ -355,10 +362,10 @@ int run_attention_bwd(bool sparse, const hilberta_config* cfg, const int32_t* sc
     Plan p{};
     hilberta::AttnArgs a{};
     bool empty = false;
-    rc = attn_setup(sparse, cfg, sched, t, 8, batch, heads, n_tot, head_dim, dtype, scale, false, p, a, empty);
+    rc = attn_setup(sparse, cfg, sched, t, 8, batch, heads, n_tot, head_dim, dtype, scale, true, p, a, empty);
     if (rc || empty) return rc;
     if (!lse) return fail(HILBERTA_EINVAL, "lse is NULL");
-    const int64_t need = bwd_ws_bytes(batch * heads, n_tot);
+    const int64_t need = bwd_ws_bytes(p, batch * heads, n_tot, head_dim);
     if (!ws) return fail(HILBERTA_EINVAL, "the backward needs a workspace of %lld bytes", (long long)need);
     if (ws_bytes < need)
         return fail(HILBERTA_ECAPACITY, "workspace of %lld bytes, %lld needed", (long long)ws_bytes,
@@ -371,17 +378,27 @@ int run_attention_bwd(bool sparse, const hilberta_config* cfg, const int32_t* sc
     g.dv = dv;
     g.delta = static_cast<float*>(ws);
     g.lse2 = static_cast<float*>(ws) + batch * heads * n_tot;
+    a.ws = static_cast<float*>(ws) + bwd_rows_bytes(batch * heads, n_tot) / 4;  // 16-byte aligned
     return hip_status(hilberta::launch_attn_bwd(a, g, (int)head_dim, static_cast<hipStream_t>(stream)),
                       "backward launch");
 }
 
-int bwd_ws_query(int64_t batch, int64_t heads, int64_t n_tot, int64_t head_dim, int dtype, int64_t* bytes) {
+int bwd_ws_query(bool sparse, const hilberta_config* cfg, int64_t batch, int64_t heads, int64_t n_tot,
+                 int64_t head_dim, int dtype, int64_t* bytes) {
     if (!bytes) return fail(HILBERTA_EINVAL, "bytes is NULL");
     if (batch < 0 || heads < 0 || n_tot < 0) return fail(HILBERTA_EINVAL, "negative size");
     if (head_dim != 64 && head_dim != 128)
         return fail(HILBERTA_EUNSUPPORTED, "head_dim %lld not in {64, 128}", (long long)head_dim);
     if (dtype != HILBERTA_BF16) return fail(HILBERTA_EUNSUPPORTED, "the backward runs in bf16 only");
-    *bytes = bwd_ws_bytes(batch * heads, n_tot);
+    Plan p{};
+    if (sparse) {
+        const Geom g = geom(cfg);
+        p = make_plan(true, g.prefix, g.tiled, g.shared_in_span, cfg->tile, n_tot, batch * heads, head_dim, dtype,
+                      true);
+    } else {
+        p = make_plan(false, 0, n_tot, 0, n_tot, n_tot, batch * heads, head_dim, dtype, true);
+    }
+    *bytes = bwd_ws_bytes(p, batch * heads, n_tot, head_dim);
     return HILBERTA_OK;
 }
 
@@ -533,7 +550,7 @@ int hilberta_attn_bwd_workspace_bytes(const hilberta_config* cfg, int64_t batch,
                                       int64_t head_dim, int dtype, int64_t* bytes) {
     int rc = check_config(cfg);
     if (rc) return rc;
-    return bwd_ws_query(batch, heads, cfg->n_txt + span_len(cfg), head_dim, dtype, bytes);
+    return bwd_ws_query(true, cfg, batch, heads, cfg->n_txt + span_len(cfg), head_dim, dtype, bytes);
 }
 
 int hilberta_attn_bwd(const hilberta_config* cfg, const int32_t* sched, const void* q, const void* k,
@@ -552,7 +569,7 @@ int hilberta_attn_bwd(const hilberta_config* cfg, const int32_t* sched, const vo
 
 int dense_attn_bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t head_dim, int dtype,
                                    int64_t* bytes) {
-    return bwd_ws_query(batch, heads, n, head_dim, dtype, bytes);
+    return bwd_ws_query(false, nullptr, batch, heads, n, head_dim, dtype, bytes);
 }
 
 int dense_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,

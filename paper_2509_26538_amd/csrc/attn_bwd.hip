@@ -71,6 +71,76 @@ __device__ __forceinline__ void store_grad(__bf16* row, const f32x16 acc[D / 32]
                            acc[dt][4 * q + 2] * mul, acc[dt][4 * q + 3] * mul);
 }
 
+// Rows that attend every key (dQ) and keys every query attends (dK, dV) are
+// split into key (query) chunks like the forward's dense rows.  Chunk c of
+// dense row r writes its unscaled sums to ws[((bh C + c) R + r) 2 + t][D]
+// (t = 0: dQ or dK, 1: dV), and bwd_sum_kernel adds the chunks up.
+template <int D>
+__device__ __forceinline__ void store_partial(const AttnArgs& a, int32_t bh, int32_t chunk, int32_t dense_row,
+                                              int t, const f32x16 acc[D / 32], int h) {
+    if (dense_row < 0 || dense_row >= a.n_dense_rows) return;
+    const int64_t slot = ((int64_t)bh * a.n_chunks + chunk) * a.n_dense_rows + dense_row;
+    float* w = a.ws + (slot * 2 + t) * D;
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<f4*>(w + 32 * dt + 8 * q + 4 * h) =
+                f4{acc[dt][4 * q], acc[dt][4 * q + 1], acc[dt][4 * q + 2], acc[dt][4 * q + 3]};
+}
+
+// Sum of the chunk partials of every dense row: dQ (pass 0) or dK and dV
+// (pass 1), scaled and written in bf16 at the row's sequence position (text
+// rows first, then the shared runs of the schedule table).  D/4 lanes per
+// row, four elements each.
+template <int D>
+__global__ void __launch_bounds__(256) bwd_sum_kernel(AttnArgs a, BwdArgs g, int pass) {
+    constexpr int LPR = D / 4;
+    constexpr int RPB = 256 / LPR;
+    const int sub = threadIdx.x % LPR;
+    const int64_t rowid = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
+    if (rowid >= (int64_t)a.n_bh * a.n_dense_rows) return;
+    const int32_t bh = (int32_t)(rowid / a.n_dense_rows);
+    const int32_t r = (int32_t)(rowid - (int64_t)bh * a.n_dense_rows);
+    int32_t seq = r;
+    if (a.sparse && r >= a.n_txt) {
+        const int32_t n_sp = min(max(a.sched[6], 0), min(a.span_cap, kMaxSpans));
+        const int32_t* tab = a.sched + 12 + 4 * a.n_tiles;
+        int32_t u = r - a.n_txt;
+        seq = -1;
+        for (int32_t s = 0; s < n_sp; ++s) {
+            const int32_t st0 = min(max(tab[2 * s], a.n_txt), a.n_tot);
+            const int32_t ln = min(max(tab[2 * s + 1], 0), a.n_tot - st0);
+            if (u < ln) {
+                seq = st0 + u;
+                break;
+            }
+            u -= ln;
+        }
+        if (seq < 0) return;
+    }
+    const int32_t b = bh / a.heads, hh = bh - b * a.heads;
+    const float scale = a.scale_log2 * 0.69314718055994530942f;
+    for (int t = 0; t < (pass == 0 ? 1 : 2); ++t) {
+        f4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int32_t c = 0; c < a.n_chunks; ++c) {
+            const int64_t slot = ((int64_t)bh * a.n_chunks + c) * a.n_dense_rows + r;
+            acc += __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.ws + (slot * 2 + t) * D) + sub);
+        }
+        __bf16* dst;
+        float mul = scale;
+        if (pass == 0) {
+            dst = reinterpret_cast<__bf16*>(g.dq) + b * a.q_sb + hh * a.q_sh + (int64_t)seq * a.q_sr;
+        } else if (t == 0) {
+            dst = reinterpret_cast<__bf16*>(g.dk) + b * a.k_sb + hh * a.k_sh + (int64_t)seq * a.k_sr;
+        } else {
+            dst = reinterpret_cast<__bf16*>(g.dv) + b * a.v_sb + hh * a.v_sh + (int64_t)seq * a.v_sr;
+            mul = 1.f;
+        }
+        store4<__bf16>(dst + 4 * sub, acc[0] * mul, acc[1] * mul, acc[2] * mul, acc[3] * mul);
+    }
+}
+
 // Direct-load offsets of one lane for a stage tensor: lane l of load j fills
 // LDS chunk p = (w IPW + j) 64 + l, i.e. row p / CPR, stored chunk p % CPR,
 // which holds global chunk (p % CPR) ^ f(row).
@@ -113,11 +183,13 @@ __global__ void __launch_bounds__(kThreads, 1) bwd_dq_kernel(AttnArgs a, BwdArgs
     const int item = remap_xcd(blockIdx.x, a.total_items);
     const int32_t bh = item / a.items_per_bh;
     const int32_t r = item - bh * a.items_per_bh;
-    const bool dense = r < a.dense_row_blocks;
+    const int32_t dense_items = a.dense_row_blocks * a.n_chunks;
+    const bool dense = r < dense_items;
     const int32_t o = load_spans<kThreads>(a, sm.sp, tid);
     const int32_t n_shared = a.sparse ? sm.sp.cum[sm.sp.n] : 0;
-    const int32_t row0 = dense ? r * kBlockMBf16 : (r - a.dense_row_blocks) * kBlockMBf16;
-    const ItemList L = item_list(a, dense, 0, row0, o, n_shared, sm.sp, sm.n_keep, wave, lane);
+    const int32_t chunk = dense ? r % a.n_chunks : 0;
+    const int32_t row0 = dense ? (r / a.n_chunks) * kBlockMBf16 : (r - dense_items) * kBlockMBf16;
+    const ItemList L = item_list(a, dense, chunk, row0, o, n_shared, sm.sp, sm.n_keep, wave, lane);
     const int nblk = (L.total + kBN - 1) / kBN;
     RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
     if (!PAD) ri.pad = false;
@@ -262,6 +334,10 @@ __global__ void __launch_bounds__(kThreads, 1) bwd_dq_kernel(AttnArgs a, BwdArgs
         wait_vmcnt<0>();
         __syncthreads();
     }
+    if (dense && a.n_chunks > 1) {
+        store_partial<D>(a, bh, chunk, ri.dense_row, 0, acc, h);
+        return;
+    }
     if (!ri.store) return;
     store_grad<D>(dqrow, acc, ri.pad ? 0.f : a.scale_log2 * 0.69314718055994530942f, h);
 }
@@ -294,11 +370,13 @@ __global__ void __launch_bounds__(kThreads, 1) bwd_dkdv_kernel(AttnArgs a, BwdAr
     const int item = remap_xcd(blockIdx.x, a.total_items);
     const int32_t bh = item / a.items_per_bh;
     const int32_t r = item - bh * a.items_per_bh;
-    const bool dense = r < a.dense_row_blocks;
+    const int32_t dense_items = a.dense_row_blocks * a.n_chunks;
+    const bool dense = r < dense_items;
     const int32_t o = load_spans<kThreads>(a, sm.sp, tid);
     const int32_t n_shared = a.sparse ? sm.sp.cum[sm.sp.n] : 0;
-    const int32_t row0 = dense ? r * kBlockMBf16 : (r - a.dense_row_blocks) * kBlockMBf16;
-    const ItemList L = item_list(a, dense, 0, row0, o, n_shared, sm.sp, sm.n_keep, wave, lane);
+    const int32_t chunk = dense ? r % a.n_chunks : 0;
+    const int32_t row0 = dense ? (r / a.n_chunks) * kBlockMBf16 : (r - dense_items) * kBlockMBf16;
+    const ItemList L = item_list(a, dense, chunk, row0, o, n_shared, sm.sp, sm.n_keep, wave, lane);
     const int nblk = (L.total + kBN - 1) / kBN;
     // this lane's key row (the item's rows are keys here)
     RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
@@ -474,6 +552,11 @@ __global__ void __launch_bounds__(kThreads, 1) bwd_dkdv_kernel(AttnArgs a, BwdAr
         }
         __syncthreads();
     }
+    if (dense && a.n_chunks > 1) {
+        store_partial<D>(a, bh, chunk, ri.dense_row, 0, acck, h);
+        store_partial<D>(a, bh, chunk, ri.dense_row, 1, accv, h);
+        return;
+    }
     if (!ri.store) return;
     store_grad<D>(dkrow, acck, ri.pad ? 0.f : a.scale_log2 * 0.69314718055994530942f, h);
     store_grad<D>(dvrow, accv, ri.pad ? 0.f : 1.f, h);
@@ -488,13 +571,19 @@ hipError_t launch_bwd_t(const AttnArgs& a, const BwdArgs& g, hipStream_t s) {
     hipLaunchKernelGGL((bwd_prep_kernel<D>), dim3((unsigned)pblocks), dim3(256), 0, s, a, g);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (a.padded) {
+    const int64_t srows = (int64_t)a.n_bh * a.n_dense_rows;
+    const unsigned sblocks = (unsigned)((srows + rpb - 1) / rpb);
+    const bool split = a.n_chunks > 1 && srows > 0;
+    if (a.padded)
         hipLaunchKernelGGL((bwd_dq_kernel<D, true>), dim3(a.total_items), dim3(kThreads), 0, s, a, g);
-        hipLaunchKernelGGL((bwd_dkdv_kernel<D, true>), dim3(a.total_items), dim3(kThreads), 0, s, a, g);
-    } else {
+    else
         hipLaunchKernelGGL((bwd_dq_kernel<D, false>), dim3(a.total_items), dim3(kThreads), 0, s, a, g);
+    if (split) hipLaunchKernelGGL((bwd_sum_kernel<D>), dim3(sblocks), dim3(256), 0, s, a, g, 0);
+    if (a.padded)
+        hipLaunchKernelGGL((bwd_dkdv_kernel<D, true>), dim3(a.total_items), dim3(kThreads), 0, s, a, g);
+    else
         hipLaunchKernelGGL((bwd_dkdv_kernel<D, false>), dim3(a.total_items), dim3(kThreads), 0, s, a, g);
-    }
+    if (split) hipLaunchKernelGGL((bwd_sum_kernel<D>), dim3(sblocks), dim3(256), 0, s, a, g, 1);
     return hipGetLastError();
 }
 

@@ -114,7 +114,7 @@ def test_sparse_backward(gpu, layout, head_dim):
                 assert np.all(g[:, :, pad] == 0)
 
 
-@pytest.mark.parametrize("n,head_dim", [(200, 64), (333, 128), (64, 128)])
+@pytest.mark.parametrize("n,head_dim", [(200, 64), (333, 128), (64, 128), (1100, 64)])
 def test_dense_backward(gpu, n, head_dim):
     q, k, v, do = inputs(n, 2, 2, head_dim, seed=n)
     got = run_dense(q, k, v, do, gpu)
