@@ -328,6 +328,48 @@ def main():
     general = {name: general_report(name) for name in ("flux-96", "flux-64x96")}
     torch.cuda.empty_cache()
 
+    # backward (training through the sparse attention): gradients of one
+    # layer's attention against the dense backward of the same shape.
+    # Algorithmic FLOPs: five products over the visited pairs (S recomputed,
+    # dP, dV, dK, dQ), 2.5x the forward's.
+    def backward_report(wname, calls):
+        bw = synth.WORKLOADS[wname]
+        bs = setup(bw)
+        hb.hilberta_schedule(bs["cfg"], 1, bs["sched"])
+        nnz = nnz_from_table(bw, bs["sched"].cpu().numpy())
+        lse = torch.empty(bw.batch, bw.heads, bw.n_tot, dtype=torch.float32, device=dev)
+        hb.hilberta_attn_fwd(bs["cfg"], bs["sched"], bs["q"], bs["k"], bs["v"], bs["o"], lse, workspace=bs["ws"])
+        dout = synth.qkv(bw.batch, bw.heads, bw.n_tot, bw.head_dim, "bf16", seed=bw.seed + 7)[0].to(dev)
+        grads = [torch.empty_like(bs["q"]) for _ in range(3)]
+        bws = torch.empty(hb.hilberta_attn_bwd_workspace_bytes(bs["cfg"], bw.batch, bw.heads, bw.head_dim,
+                                                               hb.HILBERTA_BF16), dtype=torch.uint8, device=dev)
+        call = lambda: hb.hilberta_attn_bwd(bs["cfg"], bs["sched"], bs["q"], bs["k"], bs["v"], bs["o"], dout,  # noqa: E731
+                                            lse, *grads, bws)
+        call()
+        sp = per_call(call, calls)
+        dlse = torch.empty_like(lse)
+        hb.dense_attn_fwd(bs["q"], bs["k"], bs["v"], bs["o"], dlse, workspace=bs["dws"])
+        dbws = torch.empty(hb.dense_attn_bwd_workspace_bytes(bw.batch, bw.heads, bw.n_tot, bw.head_dim,
+                                                             hb.HILBERTA_BF16), dtype=torch.uint8, device=dev)
+        dcall = lambda: hb.dense_attn_bwd(bs["q"], bs["k"], bs["v"], bs["o"], dout, dlse, *grads, dbws)  # noqa: E731
+        dcall()
+        de = per_call(dcall, max(3, calls // 10))
+        sp_ms, de_ms = statistics.median(sp), statistics.median(de)
+        fl = 10 * bw.head_dim * bw.batch * bw.heads * nnz
+        fl_dense = 10 * bw.head_dim * bw.batch * bw.heads * bw.n_tot ** 2
+        return {
+            "sparse_ms_per_call": round(sp_ms, 4),
+            "sparse_ms_p10_p90": spread(sp),
+            "sparse_tflops": round(fl / (sp_ms * 1e-3) / 1e12, 1),
+            "sparse_frac_bf16_peak": round(fl / (sp_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "dense_ms_per_call": round(de_ms, 4),
+            "dense_tflops": round(fl_dense / (de_ms * 1e-3) / 1e12, 1),
+            "speedup_vs_dense": round(de_ms / sp_ms, 2),
+        }
+
+    backward = {"flux-128": backward_report("flux-128", 20), "flux-64": backward_report("flux-64", 20)}
+    torch.cuda.empty_cache()
+
     # ------------------------------------------------------- token gather
     # cold: a 512 MB write evicts the 256 MB last-level cache before each call
     flush = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device=dev)
@@ -414,6 +456,7 @@ def main():
         "paper_table1_settings": table1,
         "attn_256": rep256,
         "general_shapes": general,
+        "backward": backward,
         "gather": gather,
         "wall_s_timed": round(wall, 3),
     }
