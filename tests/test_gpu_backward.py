@@ -168,3 +168,34 @@ def test_fullsize_sampled_rows(gpu, name, n_global):
                                                 q_rows, k_rows)
     sub = [got[0][:, heads][:, :, q_rows], got[1][:, heads][:, :, k_rows], got[2][:, heads][:, :, k_rows]]
     assert_grads(sub, list(ref), "%s rows" % name)
+
+
+def test_batch_and_strided_layout(gpu):
+    # two batch entries in Flux's [B, N, H, D] storage, seen as [B, H, N, D]
+    # views without a copy; gradients land in tensors of the same layout
+    layout = Layout(16, 16, 77, 64, 40, 4, 4)
+    q, k, v, do = inputs(layout.n_tot, 2, 3, 128, seed=21)
+    cfg, sched = make_schedule(layout, 1, gpu)
+    bnhd = lambda t: t.to(gpu).transpose(1, 2).contiguous().transpose(1, 2)  # noqa: E731
+    qd, kd, vd, dod = (bnhd(t) for t in (q, k, v, do))
+    b, h, n, d = q.shape
+    o = bnhd(torch.zeros_like(q))
+    lse = torch.empty(b, h, n, dtype=torch.float32, device=gpu)
+    hb.hilberta_attn_fwd(cfg, sched, qd, kd, vd, o, lse)
+    grads = [bnhd(torch.full_like(q, float("nan"))) for _ in range(3)]
+    assert grads[0].stride() == qd.stride() and qd.stride(2) == h * d
+    bws = torch.empty(hb.hilberta_attn_bwd_workspace_bytes(cfg, b, h, d, hb.HILBERTA_BF16), dtype=torch.uint8,
+                      device=gpu)
+    hb.hilberta_attn_bwd(cfg, sched, qd, kd, vd, o, dod, lse, *grads, bws)
+    torch.cuda.synchronize()
+    got = [g.cpu().to(torch.float64).numpy() for g in grads]
+    ref = oracle(q, k, v, do, lambda rows: schedule.mask_rows(layout, 1, rows))
+    assert_grads(got, ref, "strided")
+
+
+def test_empty_batch_is_a_no_op(gpu):
+    layout = Layout(16, 16, 0, 64, 32, 4, 4)
+    cfg, sched = make_schedule(layout, 0, gpu)
+    z = torch.empty(0, 2, layout.n_tot, 64, dtype=torch.bfloat16, device=gpu)
+    lse = torch.empty(0, 2, layout.n_tot, dtype=torch.float32, device=gpu)
+    hb.hilberta_attn_bwd(cfg, sched, z, z, z, z, z, lse, z, z, z, None)
