@@ -23,8 +23,8 @@
 // whole sequence.  Each stage tensor is staged through LDS by direct loads
 // in the layout its reads need (fk for whole-row A operands, fv for the
 // transposing reads; Q, dO and K are read both ways and staged twice).
-// Their operands and accumulators take most of the register file, so each
-// SIMD runs one wavefront.
+// Stages hold 32 list rows, so that the double-buffered stages of two
+// workgroups fit a CU's LDS and each SIMD interleaves two wavefronts.
 #include "bf16_stage.hpp"
 
 namespace hilberta {
@@ -141,38 +141,27 @@ __global__ void __launch_bounds__(256) bwd_sum_kernel(AttnArgs a, BwdArgs g, int
     }
 }
 
-// Direct-load offsets of one lane for a stage tensor: lane l of load j fills
-// LDS chunk p = (w IPW + j) 64 + l, i.e. row p / CPR, stored chunk p % CPR,
-// which holds global chunk (p % CPR) ^ f(row).
-template <int D>
-struct LaneLoads {
-    int32_t srow[Geo<D>::IPW], colk[Geo<D>::IPW], colv[Geo<D>::IPW];
-    __device__ __forceinline__ void init(int wave, int lane) {
-#pragma unroll
-        for (int j = 0; j < Geo<D>::IPW; ++j) {
-            const int p = (wave * Geo<D>::IPW + j) * 64 + lane;
-            srow[j] = p / Geo<D>::CPR;
-            colk[j] = ((p % Geo<D>::CPR) ^ Geo<D>::fk(srow[j])) * 16;
-            colv[j] = ((p % Geo<D>::CPR) ^ Geo<D>::fv(srow[j])) * 16;
-        }
-    }
-};
-
 // ---------------------------------------------------------------------- dQ
+constexpr int kBQ = 32;  // list rows per stage
+
 template <int D>
 struct SmemDq {
-    alignas(16) uint8_t k[2][Geo<D>::STAGEB];   // fk: A operand of S^T
-    alignas(16) uint8_t kt[2][Geo<D>::STAGEB];  // fv: transposed A operand of dQ^T
-    alignas(16) uint8_t v[2][Geo<D>::STAGEB];   // fk: A operand of dP^T
-    alignas(16) int32_t info[2][kBN];
+    static constexpr int SB = kBQ * Geo<D>::ROWB;
+    alignas(16) uint8_t k[2][SB];   // fk: A operand of S^T
+    alignas(16) uint8_t kt[2][SB];  // fv: transposed A operand of dQ^T
+    alignas(16) uint8_t v[2][SB];   // fk: A operand of dP^T
+    alignas(16) int32_t info[2][kBQ];
     Spans sp;
     int32_t n_keep;
     int32_t slow[2];
 };
 
 template <int D, bool PAD>
-__global__ void __launch_bounds__(kThreads, 1) bwd_dq_kernel(AttnArgs a, BwdArgs g) {
+__global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs g) {
     using G = Geo<D>;
+    constexpr int SB = SmemDq<D>::SB;
+    constexpr int IPW = SB / 1024 / 4 > 0 ? SB / 1024 / 4 : 1;
+    static_assert(SB == IPW * 1024 * 4, "stage of whole 1 KB loads per wavefront");
     __shared__ SmemDq<D> sm;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -190,7 +179,7 @@ __global__ void __launch_bounds__(kThreads, 1) bwd_dq_kernel(AttnArgs a, BwdArgs
     const int32_t chunk = dense ? r % a.n_chunks : 0;
     const int32_t row0 = dense ? (r / a.n_chunks) * kBlockMBf16 : (r - dense_items) * kBlockMBf16;
     const ItemList L = item_list(a, dense, chunk, row0, o, n_shared, sm.sp, sm.n_keep, wave, lane);
-    const int nblk = (L.total + kBN - 1) / kBN;
+    const int nblk = (L.total + kBQ - 1) / kBQ;
     RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
     if (!PAD) ri.pad = false;
 
@@ -220,52 +209,60 @@ __global__ void __launch_bounds__(kThreads, 1) bwd_dq_kernel(AttnArgs a, BwdArgs
     const __amdgpu_buffer_rsrc_t krs = slice_rsrc(kbase, a.n_tot, a.k_sr, D, 2);
     const __amdgpu_buffer_rsrc_t vrs = slice_rsrc(vbase, a.n_tot, a.v_sr, D, 2);
     const int32_t krow_b = (int32_t)(a.k_sr * 2), vrow_b = (int32_t)(a.v_sr * 2);
-    LaneLoads<D> ll;
-    ll.init(wave, lane);
-    const uint32_t k0 = lds_addr(&sm.k[0][wave * G::IPW * 1024]);
-    const uint32_t kt0 = lds_addr(&sm.kt[0][wave * G::IPW * 1024]);
-    const uint32_t v0l = lds_addr(&sm.v[0][wave * G::IPW * 1024]);
+    // direct loads: lane l of load j fills LDS chunk p = (w IPW + j) 64 + l
+    // of the stage, i.e. row p / CPR, stored chunk p % CPR, which holds
+    // global chunk (p % CPR) ^ f(row)
+    int32_t srow[IPW], colk[IPW], colv[IPW];
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+        const int p = (wave * IPW + j) * 64 + lane;
+        srow[j] = p / G::CPR;
+        colk[j] = ((p % G::CPR) ^ G::fk(srow[j])) * 16;
+        colv[j] = ((p % G::CPR) ^ G::fv(srow[j])) * 16;
+    }
+    const uint32_t k0 = lds_addr(&sm.k[0][wave * IPW * 1024]);
+    const uint32_t kt0 = lds_addr(&sm.kt[0][wave * IPW * 1024]);
+    const uint32_t v0l = lds_addr(&sm.v[0][wave * IPW * 1024]);
 
     auto stage_fast = [&](int32_t i) -> bool {
-        const int32_t v0 = i * kBN;
-        return L.total - v0 >= kBN && !(L.label_mask && v0 + kBN > L.b2);
+        const int32_t v0 = i * kBQ;
+        return L.total - v0 >= kBQ && !(L.label_mask && v0 + kBQ > L.b2);
     };
     auto load_stage = [&](int32_t i, int buf) {
-        const int32_t v0 = i * kBN;
-        const int32_t cnt = min(kBN, L.total - v0);
+        const int32_t v0 = i * kBQ;
+        const int32_t cnt = min(kBQ, L.total - v0);
         int32_t base = -1;
         if (v0 + cnt <= L.b1) base = L.s0 + v0;
         else if (v0 >= L.b2 && v0 + cnt <= L.b3) base = L.sa + (v0 - L.b2);
         else if (v0 >= L.b3) base = L.sb + (v0 - L.b3);
         if (PAD) {
-            const int32_t v = v0 + lane;
+            const int32_t v = lane < kBQ ? v0 + lane : L.total;
             const int32_t seq = v >= L.total ? 0 : base >= 0 ? base + lane
                                                             : list_seq(v, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
             const int32_t inf = entry_info<true>(a, L, v, seq, o, sm.sp);
             const bool none = __builtin_amdgcn_ballot_w64(inf != kKeyInvalid) == 0;
             if (wave == 0) {
-                sm.info[buf][lane] = inf;
-                const bool slow = __builtin_amdgcn_ballot_w64(inf != kKeyAll) != 0;
+                if (lane < kBQ) sm.info[buf][lane] = inf;
+                const bool slow = __builtin_amdgcn_ballot_w64(lane < kBQ && inf != kKeyAll) != 0;
                 if (lane == 0) sm.slow[buf] = none ? 2 : slow ? 1 : 0;
             }
             if (none) return;
         }
-        const uint32_t off = buf * G::STAGEB;
+        const uint32_t off = buf * SB;
 #pragma unroll
-        for (int j = 0; j < G::IPW; ++j) {
+        for (int j = 0; j < IPW; ++j) {
             int32_t key;
-            if (base >= 0 && cnt == kBN) {
-                key = base + ll.srow[j];
+            if (base >= 0 && cnt == kBQ) {
+                key = base + srow[j];
             } else {
-                // absent rows of a ragged stage re-read a present row (masked)
-                const int32_t rr = min(ll.srow[j], cnt - 1);
+                const int32_t rr = min(srow[j], cnt - 1);
                 key = base >= 0 ? base + rr : list_seq(v0 + rr, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
             }
-            dma16(krs, k0 + off + j * 1024, key * krow_b + ll.colk[j]);
-            dma16(krs, kt0 + off + j * 1024, key * krow_b + ll.colv[j]);
-            dma16(vrs, v0l + off + j * 1024, key * vrow_b + ll.colk[j]);
+            dma16(krs, k0 + off + j * 1024, key * krow_b + colk[j]);
+            dma16(krs, kt0 + off + j * 1024, key * krow_b + colv[j]);
+            dma16(vrs, v0l + off + j * 1024, key * vrow_b + colk[j]);
         }
-        if (!PAD && !stage_fast(i) && tid < kBN) {
+        if (!PAD && !stage_fast(i) && tid < kBQ) {
             const int32_t v = v0 + tid;
             const int32_t seq = v >= L.total ? 0 : list_seq(v, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
             sm.info[buf][tid] = entry_info<false>(a, L, v, seq, o, sm.sp);
@@ -289,43 +286,35 @@ __global__ void __launch_bounds__(kThreads, 1) bwd_dq_kernel(AttnArgs a, BwdArgs
         if (!PAD || sm.slow[buf] != 2) {
             const uint8_t* kb_ = sm.k[buf];
             const uint8_t* vb_ = sm.v[buf];
-            // S^T = K Q^T and dP^T = V dO^T: register e of s[kt], dp[kt]
-            // holds key 32 kt + 8 (e/4) + 4 h + e%4 against this lane's row
-            f32x16 s[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
+            // S^T = K Q^T and dP^T = V dO^T: register e holds key
+            // 8 (e/4) + 4 h + e%4 against this lane's row
+            f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
-            for (int kc = 0; kc < D / 16; ++kc)
-#pragma unroll
-                for (int kt = 0; kt < 2; ++kt) {
-                    const int ad = (ka ^ (32 * kc)) + kt * 32 * G::ROWB;
-                    s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(kb_ + ad),
-                                                                    q[kc], s[kt], 0, 0, 0);
-                    dp[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(vb_ + ad),
-                                                                     dov[kc], dp[kt], 0, 0, 0);
-                }
+            for (int kc = 0; kc < D / 16; ++kc) {
+                const int ad = ka ^ (32 * kc);
+                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(kb_ + ad), q[kc], s, 0, 0, 0);
+                dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(vb_ + ad), dov[kc], dp, 0,
+                                                             0, 0);
+            }
             if (PAD ? sm.slow[buf] != 0 : !stage_fast(i)) {
 #pragma unroll
-                for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) {
-                        const int32_t inf = sm.info[buf][32 * kt + 8 * (e >> 2) + 4 * h + (e & 3)];
-                        s[kt][e] = (inf == kKeyAll || inf == ri.label) ? s[kt][e] : -INFINITY;
-                    }
+                for (int e = 0; e < 16; ++e) {
+                    const int32_t inf = sm.info[buf][8 * (e >> 2) + 4 * h + (e & 3)];
+                    s[e] = (inf == kKeyAll || inf == ri.label) ? s[e] : -INFINITY;
+                }
             }
-            // dS = P (dP - Dlt), rounded to bf16 in the key order of the
-            // transposed K operand: chunk cc, register j = key 16 cc + 8 (j/4)
-            // + 4 h + j%4
-            bf16x8 ds[4];
+            bf16x8 ds[2];
 #pragma unroll
-            for (int cc = 0; cc < 4; ++cc)
+            for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    const int e = 8 * (cc & 1) + j;
-                    const float pe = __builtin_amdgcn_exp2f(fmaf(s[cc >> 1][e], c, -lse2));
-                    ds[cc][j] = (__bf16)(pe * (dp[cc >> 1][e] - dlt));
+                    const int e = 8 * cc + j;
+                    const float pe = __builtin_amdgcn_exp2f(fmaf(s[e], c, -lse2));
+                    ds[cc][j] = (__bf16)(pe * (dp[e] - dlt));
                 }
             const uint8_t* ktb = sm.kt[buf];
 #pragma unroll
-            for (int cc = 0; cc < 4; ++cc)
+            for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
                 for (int dt = 0; dt < D / 32; ++dt)
                     acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(ktb, va, cc, dt), ds[cc], acc[dt],
@@ -345,21 +334,25 @@ __global__ void __launch_bounds__(kThreads, 1) bwd_dq_kernel(AttnArgs a, BwdArgs
 // -------------------------------------------------------------------- dK dV
 template <int D>
 struct SmemDkdv {
-    alignas(16) uint8_t q[2][Geo<D>::STAGEB];   // fk: A operand of S
-    alignas(16) uint8_t qt[2][Geo<D>::STAGEB];  // fv: transposed A operand of dK^T
-    alignas(16) uint8_t d[2][Geo<D>::STAGEB];   // fk: dO, A operand of dP
-    alignas(16) uint8_t dt[2][Geo<D>::STAGEB];  // fv: dO, transposed A operand of dV^T
-    alignas(16) float lse2[2][kBN];
-    alignas(16) float dlt[2][kBN];
-    alignas(16) int32_t info[2][kBN];
+    static constexpr int SB = kBQ * Geo<D>::ROWB;
+    alignas(16) uint8_t q[2][SB];   // fk: A operand of S
+    alignas(16) uint8_t qt[2][SB];  // fv: transposed A operand of dK^T
+    alignas(16) uint8_t d[2][SB];   // fk: dO, A operand of dP
+    alignas(16) uint8_t dt[2][SB];  // fv: dO, transposed A operand of dV^T
+    alignas(16) float lse2[2][kBQ];
+    alignas(16) float dlt[2][kBQ];
+    alignas(16) int32_t info[2][kBQ];
     Spans sp;
     int32_t n_keep;
     int32_t slow[2];
 };
 
 template <int D, bool PAD>
-__global__ void __launch_bounds__(kThreads, 1) bwd_dkdv_kernel(AttnArgs a, BwdArgs g) {
+__global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdArgs g) {
     using G = Geo<D>;
+    constexpr int SB = SmemDkdv<D>::SB;
+    constexpr int IPW = SB / 1024 / 4 > 0 ? SB / 1024 / 4 : 1;
+    static_assert(SB == IPW * 1024 * 4, "stage of whole 1 KB loads per wavefront");
     __shared__ SmemDkdv<D> sm;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -377,8 +370,7 @@ __global__ void __launch_bounds__(kThreads, 1) bwd_dkdv_kernel(AttnArgs a, BwdAr
     const int32_t chunk = dense ? r % a.n_chunks : 0;
     const int32_t row0 = dense ? (r / a.n_chunks) * kBlockMBf16 : (r - dense_items) * kBlockMBf16;
     const ItemList L = item_list(a, dense, chunk, row0, o, n_shared, sm.sp, sm.n_keep, wave, lane);
-    const int nblk = (L.total + kBN - 1) / kBN;
-    // this lane's key row (the item's rows are keys here)
+    const int nblk = (L.total + kBQ - 1) / kBQ;
     RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
     if (!PAD) ri.pad = false;
 
@@ -412,37 +404,40 @@ __global__ void __launch_bounds__(kThreads, 1) bwd_dkdv_kernel(AttnArgs a, BwdAr
     const int32_t qrow_b = (int32_t)(a.q_sr * 2), drow_b = (int32_t)(a.o_sr * 2);
     const float* lse2_bh = g.lse2 + (int64_t)bh * a.n_tot;
     const float* dlt_bh = g.delta + (int64_t)bh * a.n_tot;
-    LaneLoads<D> ll;
-    ll.init(wave, lane);
-    const uint32_t q0 = lds_addr(&sm.q[0][wave * G::IPW * 1024]);
-    const uint32_t qt0 = lds_addr(&sm.qt[0][wave * G::IPW * 1024]);
-    const uint32_t d0 = lds_addr(&sm.d[0][wave * G::IPW * 1024]);
-    const uint32_t dt0 = lds_addr(&sm.dt[0][wave * G::IPW * 1024]);
+    int32_t srow[IPW], colk[IPW], colv[IPW];
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+        const int p = (wave * IPW + j) * 64 + lane;
+        srow[j] = p / G::CPR;
+        colk[j] = ((p % G::CPR) ^ G::fk(srow[j])) * 16;
+        colv[j] = ((p % G::CPR) ^ G::fv(srow[j])) * 16;
+    }
+    const uint32_t q0 = lds_addr(&sm.q[0][wave * IPW * 1024]);
+    const uint32_t qt0 = lds_addr(&sm.qt[0][wave * IPW * 1024]);
+    const uint32_t d0 = lds_addr(&sm.d[0][wave * IPW * 1024]);
+    const uint32_t dt0 = lds_addr(&sm.dt[0][wave * IPW * 1024]);
 
-    // per-query LSE and Dlt of the stage being loaded: read into registers
-    // by wavefront 0 (lane = list entry) and written to LDS before the
-    // barrier that publishes the stage
     float nl = 0.f, nd = 0.f;
     auto stage_fast = [&](int32_t i) -> bool {
-        const int32_t v0 = i * kBN;
-        return L.total - v0 >= kBN && !(L.label_mask && v0 + kBN > L.b2);
+        const int32_t v0 = i * kBQ;
+        return L.total - v0 >= kBQ && !(L.label_mask && v0 + kBQ > L.b2);
     };
     auto load_stage = [&](int32_t i, int buf) {
-        const int32_t v0 = i * kBN;
-        const int32_t cnt = min(kBN, L.total - v0);
+        const int32_t v0 = i * kBQ;
+        const int32_t cnt = min(kBQ, L.total - v0);
         int32_t base = -1;
         if (v0 + cnt <= L.b1) base = L.s0 + v0;
         else if (v0 >= L.b2 && v0 + cnt <= L.b3) base = L.sa + (v0 - L.b2);
         else if (v0 >= L.b3) base = L.sb + (v0 - L.b3);
-        const int32_t v = v0 + lane;
+        const int32_t v = lane < kBQ ? v0 + lane : L.total;
         const int32_t seq = v >= L.total ? 0 : base >= 0 ? base + lane
                                                         : list_seq(v, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
         if (PAD) {
             const int32_t inf = entry_info<true>(a, L, v, seq, o, sm.sp);
             const bool none = __builtin_amdgcn_ballot_w64(inf != kKeyInvalid) == 0;
             if (wave == 0) {
-                sm.info[buf][lane] = inf;
-                const bool slow = __builtin_amdgcn_ballot_w64(inf != kKeyAll) != 0;
+                if (lane < kBQ) sm.info[buf][lane] = inf;
+                const bool slow = __builtin_amdgcn_ballot_w64(lane < kBQ && inf != kKeyAll) != 0;
                 if (lane == 0) sm.slow[buf] = none ? 2 : slow ? 1 : 0;
             }
             if (none) return;
@@ -451,22 +446,22 @@ __global__ void __launch_bounds__(kThreads, 1) bwd_dkdv_kernel(AttnArgs a, BwdAr
             nl = lse2_bh[seq];
             nd = dlt_bh[seq];
         }
-        const uint32_t off = buf * G::STAGEB;
+        const uint32_t off = buf * SB;
 #pragma unroll
-        for (int j = 0; j < G::IPW; ++j) {
+        for (int j = 0; j < IPW; ++j) {
             int32_t qs;
-            if (base >= 0 && cnt == kBN) {
-                qs = base + ll.srow[j];
+            if (base >= 0 && cnt == kBQ) {
+                qs = base + srow[j];
             } else {
-                const int32_t rr = min(ll.srow[j], cnt - 1);
+                const int32_t rr = min(srow[j], cnt - 1);
                 qs = base >= 0 ? base + rr : list_seq(v0 + rr, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
             }
-            dma16(qrs, q0 + off + j * 1024, qs * qrow_b + ll.colk[j]);
-            dma16(qrs, qt0 + off + j * 1024, qs * qrow_b + ll.colv[j]);
-            dma16(drs, d0 + off + j * 1024, qs * drow_b + ll.colk[j]);
-            dma16(drs, dt0 + off + j * 1024, qs * drow_b + ll.colv[j]);
+            dma16(qrs, q0 + off + j * 1024, qs * qrow_b + colk[j]);
+            dma16(qrs, qt0 + off + j * 1024, qs * qrow_b + colv[j]);
+            dma16(drs, d0 + off + j * 1024, qs * drow_b + colk[j]);
+            dma16(drs, dt0 + off + j * 1024, qs * drow_b + colv[j]);
         }
-        if (!PAD && !stage_fast(i) && tid < kBN) sm.info[buf][tid] = entry_info<false>(a, L, v, seq, o, sm.sp);
+        if (!PAD && !stage_fast(i) && tid < kBQ) sm.info[buf][tid] = entry_info<false>(a, L, v, seq, o, sm.sp);
     };
 
     const int ka = row_base<D>(lane);
@@ -482,7 +477,7 @@ __global__ void __launch_bounds__(kThreads, 1) bwd_dkdv_kernel(AttnArgs a, BwdAr
     wait_vmcnt<0>();
     load_stage(0, 0);
     wait_vmcnt<0>();
-    if (wave == 0) {
+    if (wave == 0 && lane < kBQ) {
         sm.lse2[0][lane] = nl;
         sm.dlt[0][lane] = nd;
     }
@@ -493,50 +488,43 @@ __global__ void __launch_bounds__(kThreads, 1) bwd_dkdv_kernel(AttnArgs a, BwdAr
         if (!PAD || sm.slow[buf] != 2) {
             const uint8_t* qb = sm.q[buf];
             const uint8_t* db = sm.d[buf];
-            // S = Q K^T and dP = dO V^T: register e of s[kt], dp[kt] holds
-            // query 32 kt + 8 (e/4) + 4 h + e%4 against this lane's key
-            f32x16 s[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
+            // S = Q K^T and dP = dO V^T: register e holds query
+            // 8 (e/4) + 4 h + e%4 against this lane's key
+            f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
-            for (int kc = 0; kc < D / 16; ++kc)
-#pragma unroll
-                for (int kt = 0; kt < 2; ++kt) {
-                    const int ad = (ka ^ (32 * kc)) + kt * 32 * G::ROWB;
-                    s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(qb + ad),
-                                                                    kr[kc], s[kt], 0, 0, 0);
-                    dp[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(db + ad),
-                                                                     vr[kc], dp[kt], 0, 0, 0);
-                }
+            for (int kc = 0; kc < D / 16; ++kc) {
+                const int ad = ka ^ (32 * kc);
+                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(qb + ad), kr[kc], s, 0, 0, 0);
+                dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(db + ad), vr[kc], dp, 0, 0,
+                                                             0);
+            }
             if (PAD ? sm.slow[buf] != 0 : !stage_fast(i)) {
 #pragma unroll
-                for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) {
-                        const int32_t inf = sm.info[buf][32 * kt + 8 * (e >> 2) + 4 * h + (e & 3)];
-                        s[kt][e] = (inf == kKeyAll || inf == ri.label) ? s[kt][e] : -INFINITY;
-                    }
+                for (int e = 0; e < 16; ++e) {
+                    const int32_t inf = sm.info[buf][8 * (e >> 2) + 4 * h + (e & 3)];
+                    s[e] = (inf == kKeyAll || inf == ri.label) ? s[e] : -INFINITY;
+                }
             }
-            // P and dS per query, in the order of the transposed operands
-            bf16x8 pb[4], ds[4];
+            bf16x8 pb[2], ds[2];
 #pragma unroll
-            for (int cc = 0; cc < 4; ++cc)
+            for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
                 for (int j4 = 0; j4 < 2; ++j4) {
-                    const int kt = cc >> 1, g4 = 2 * (cc & 1) + j4;
-                    const int q0i = 32 * kt + 8 * g4 + 4 * h;
-                    const f4 l4 = *reinterpret_cast<const f4*>(&sm.lse2[buf][q0i]);
-                    const f4 d4 = *reinterpret_cast<const f4*>(&sm.dlt[buf][q0i]);
+                    const int g4 = 2 * cc + j4;
+                    const f4 l4 = *reinterpret_cast<const f4*>(&sm.lse2[buf][8 * g4 + 4 * h]);
+                    const f4 d4 = *reinterpret_cast<const f4*>(&sm.dlt[buf][8 * g4 + 4 * h]);
 #pragma unroll
                     for (int t = 0; t < 4; ++t) {
                         const int e = 4 * g4 + t;
-                        const float pe = __builtin_amdgcn_exp2f(fmaf(s[kt][e], c, -l4[t]));
+                        const float pe = __builtin_amdgcn_exp2f(fmaf(s[e], c, -l4[t]));
                         pb[cc][4 * j4 + t] = (__bf16)pe;
-                        ds[cc][4 * j4 + t] = (__bf16)(pe * (dp[kt][e] - d4[t]));
+                        ds[cc][4 * j4 + t] = (__bf16)(pe * (dp[e] - d4[t]));
                     }
                 }
             const uint8_t* dtb = sm.dt[buf];
             const uint8_t* qtb = sm.qt[buf];
 #pragma unroll
-            for (int cc = 0; cc < 4; ++cc)
+            for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
                 for (int dt = 0; dt < D / 32; ++dt) {
                     accv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(dtb, va, cc, dt), pb[cc],
@@ -546,7 +534,7 @@ __global__ void __launch_bounds__(kThreads, 1) bwd_dkdv_kernel(AttnArgs a, BwdAr
                 }
         }
         wait_vmcnt<0>();
-        if (wave == 0 && i + 1 < nblk) {
+        if (wave == 0 && lane < kBQ && i + 1 < nblk) {
             sm.lse2[buf ^ 1][lane] = nl;
             sm.dlt[buf ^ 1][lane] = nd;
         }
