@@ -166,6 +166,27 @@ def main():
     attn_avg_ms = statistics.fmean(attn_ms)
     achieved = sum(attn_flops) / (sum(attn_ms) * 1e-3) / 1e12
 
+    # the same step captured once as a HIP graph and replayed: every call of
+    # the path is a kernel launch on the caller's stream, so nothing stops a
+    # capture (reported beside the eager step, which is the measured value)
+    gstream = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(gstream):
+        step(False)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph, stream=gstream):
+        step(False)
+    graph.replay()
+    torch.cuda.synchronize()
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g0.record()
+    for _ in range(args.steps):
+        graph.replay()
+    g1.record()
+    torch.cuda.synchronize()
+    graph_ms_step = g0.elapsed_time(g1) / args.steps
+    del graph
+
     # ------------------------------------------------------- per-call rows
     def spread(xs):
         xs = sorted(xs)
@@ -424,6 +445,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "graph_replay_ms_per_step": round(graph_ms_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
