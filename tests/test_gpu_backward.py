@@ -97,6 +97,8 @@ LAYOUTS = [
     Layout(16, 16, 7, 48, 12, 4, 4, moved=True),
     Layout(12, 16, 3, 64, 16, 4, 4),       # general shape: padding
     Layout(33, 20, 130, 512, 128, 6, 4),   # general shape, ragged
+    Layout(16, 16, 0, 64, 16, 0, 0),       # no text, no shared region: no dense rows
+    Layout(2, 2, 1, 1, 1, 1, 1),           # smallest grid, one-token tiles
 ]
 
 
