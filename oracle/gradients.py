@@ -102,3 +102,4 @@ def masked_attention_grads_rows(q, k, v, do, mask_fn, q_rows, k_rows, scale=None
         dk += scale * np.matmul(np.swapaxes(ds, -1, -2), q[:, :, rows])
         dv += np.matmul(np.swapaxes(pk, -1, -2), do[:, :, rows])
     return dq, dk, dv
+
