@@ -85,57 +85,9 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
     const int32_t row0 = dense ? (r / a.n_chunks) * kBlockMBf16 : (r - dense_items) * kBlockMBf16;
 
     // ------------------------------------------------------------ key list
-    int32_t b1, b2, b3, total, s0, sa, sb;
-    bool label_mask = false;
-    if (dense) {
-        s0 = chunk * a.chunk_keys;
-        total = min(a.chunk_keys, a.n_tot - s0);
-        b1 = b2 = b3 = total;
-        sa = sb = 0;
-    } else {
-        // tiles covering the rows: in the slid coordinate t = (p + o) mod
-        // N_img the rows are a cyclic run from t0 that meets labels q1,
-        // q1 + 1, ... (mod T); a run as long as the image meets all T
-        const int32_t p_last = min(a.n_img, row0 + kBlockMBf16) - 1;
-        const int32_t t0 = (row0 + o) % a.n_img;
-        const int32_t q1 = t0 / a.tile;
-        const int32_t n_lab = min(a.n_tiles, (t0 + p_last - row0) / a.tile - q1 + 1);
-        label_mask = n_lab > 1;
-        const int32_t r_start = (int32_t)(((int64_t)q1 * a.tile - o + a.n_img) % a.n_img);
-        const int32_t r_len = min(n_lab * a.tile, a.n_img);
-        const int32_t len_a = min(r_len, a.n_img - r_start);
-        // keep the shared tokens outside [r_start, r_start + r_len) (cyclic):
-        // those inside are keys of the tile segment already.  One wavefront
-        // compacts the map in place, in order.
-        if (wave == 0) {
-            int32_t w = 0;
-            for (int32_t u0 = 0; u0 < n_shared; u0 += 64) {
-                const int32_t u = u0 + lane;
-                int32_t seq = 0;
-                bool keep = false;
-                if (u < n_shared) {
-                    seq = sm.sp.map[u];
-                    const int32_t rel = (seq - a.n_txt - r_start + a.n_img) % a.n_img;
-                    keep = rel >= r_len;
-                }
-                const uint64_t bal = __builtin_amdgcn_ballot_w64(keep);
-                const int32_t before = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
-                                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
-                if (keep) sm.sp.map[w + before] = seq;
-                w += __builtin_popcountll(bal);
-            }
-            if (lane == 0) sm.n_keep = w;
-        }
-        __syncthreads();
-        const int32_t n_keep = sm.n_keep;
-        s0 = 0;
-        b1 = a.n_txt;
-        b2 = b1 + n_keep;
-        b3 = b2 + len_a;
-        total = b2 + r_len;
-        sa = a.n_txt + r_start;
-        sb = a.n_txt;
-    }
+    const ItemList L = item_list(a, dense, chunk, row0, o, n_shared, sm.sp, sm.n_keep, wave, lane);
+    const int32_t b1 = L.b1, b2 = L.b2, b3 = L.b3, total = L.total, s0 = L.s0, sa = L.sa, sb = L.sb;
+    const bool label_mask = L.label_mask;
     const int nblk = (total + kBN - 1) / kBN;
     RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
     if (!PAD) ri.pad = false;
@@ -198,15 +150,8 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
             // each knows without a barrier whether the stage holds any key
             // at all; wavefront 0 publishes the per-key masks
             const int32_t v = v0 + lane;
-            int32_t inf = kKeyInvalid;
-            if (v < total) {
-                const int32_t seq = base >= 0 ? base + lane : list_seq(v, b1, b2, b3, s0, sa, sb, sm.sp);
-                if (!seq_padding(a, seq)) {
-                    inf = kKeyAll;
-                    if (label_mask && v >= b2 && !is_shared_seq(sm.sp, seq))
-                        inf = tile_label(seq - a.n_txt, o, a.tile, a.n_img);
-                }
-            }
+            const int32_t seq = v >= total ? 0 : base >= 0 ? base + lane : list_seq(v, b1, b2, b3, s0, sa, sb, sm.sp);
+            const int32_t inf = entry_info<true>(a, L, v, seq, o, sm.sp);
             const bool none = __builtin_amdgcn_ballot_w64(inf != kKeyInvalid) == 0;
             if (wave == 0) {
                 sm.info[buf][lane] = inf;
@@ -235,15 +180,8 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
         }
         if (!PAD && !stage_fast(i) && tid < kBN) {
             const int32_t v = v0 + tid;
-            int32_t inf = kKeyInvalid;
-            if (v < total) {
-                inf = kKeyAll;
-                if (label_mask && v >= b2) {
-                    const int32_t seq = list_seq(v, b1, b2, b3, s0, sa, sb, sm.sp);
-                    if (!is_shared_seq(sm.sp, seq)) inf = tile_label(seq - a.n_txt, o, a.tile, a.n_img);
-                }
-            }
-            sm.info[buf][tid] = inf;
+            const int32_t seq = v >= total ? 0 : list_seq(v, b1, b2, b3, s0, sa, sb, sm.sp);
+            sm.info[buf][tid] = entry_info<false>(a, L, v, seq, o, sm.sp);
         }
     };
 
