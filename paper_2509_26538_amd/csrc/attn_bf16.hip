@@ -48,6 +48,8 @@
 // stores its empty-softmax rows without visiting any key.
 #include "bf16_stage.hpp"
 
+#include <type_traits>
+
 namespace hilberta {
 namespace {
 
@@ -211,8 +213,10 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
     wait_vmcnt<0>();
     __syncthreads();
 
-    for (int32_t i = 0; i < nblk; ++i) {
-        const int buf = i & 1;
+    // one stage; the buffer index is a compile-time constant (the loop
+    // below runs stages in pairs), so LDS addresses carry it as an immediate
+    auto stage = [&](int32_t i, auto buf_c) {
+        constexpr int buf = decltype(buf_c)::value;
         if (i + 1 < nblk) load_stage(i + 1, buf ^ 1);
         // padded spans: sm.slow is 0 (no masks), 1 (per-key masks) or 2
         // (only padding keys: the stage is skipped)
@@ -257,19 +261,21 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
                         s[kt][e] = (inf == kKeyAll || inf == ri.label) ? s[kt][e] : -INFINITY;
                     }
             }
-            // row max over the 64 keys: a tree of three-way maxima
+            // row max over the 64 keys: a tree of three-way maxima (IEEE
+            // maximum, which needs no canonicalising of the MFMA results; a
+            // NaN score would reach the output through exp2 either way)
             float t3[11];
 #pragma unroll
             for (int g = 0; g < 5; ++g) {
-                t3[g] = fmaxf(fmaxf(s[0][3 * g], s[0][3 * g + 1]), s[0][3 * g + 2]);
-                t3[5 + g] = fmaxf(fmaxf(s[1][3 * g], s[1][3 * g + 1]), s[1][3 * g + 2]);
+                t3[g] = vmax(vmax(s[0][3 * g], s[0][3 * g + 1]), s[0][3 * g + 2]);
+                t3[5 + g] = vmax(vmax(s[1][3 * g], s[1][3 * g + 1]), s[1][3 * g + 2]);
             }
-            t3[10] = fmaxf(s[0][15], s[1][15]);
-            const float u0 = fmaxf(fmaxf(t3[0], t3[1]), t3[2]);
-            const float u1 = fmaxf(fmaxf(t3[3], t3[4]), t3[5]);
-            const float u2 = fmaxf(fmaxf(t3[6], t3[7]), t3[8]);
-            const float u3 = fmaxf(t3[9], t3[10]);
-            const float mx = half_max(fmaxf(fmaxf(u0, u1), fmaxf(u2, u3))) * c;
+            t3[10] = vmax(s[0][15], s[1][15]);
+            const float u0 = vmax(vmax(t3[0], t3[1]), t3[2]);
+            const float u1 = vmax(vmax(t3[3], t3[4]), t3[5]);
+            const float u2 = vmax(vmax(t3[6], t3[7]), t3[8]);
+            const float u3 = vmax(t3[9], t3[10]);
+            const float mx = half_vmax(vmax(vmax(u0, u1), vmax(u2, u3))) * c;
             if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f)) {
                 const float m_new = fmaxf(m_run, mx);
                 // a row with every key masked so far keeps -inf: leave it alone
@@ -302,6 +308,10 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
         // wavefront must be done with this buffer before it is refilled
         wait_vmcnt<0>();
         __syncthreads();
+    };
+    for (int32_t i = 0; i < nblk; i += 2) {
+        stage(i, std::integral_constant<int, 0>{});
+        if (i + 1 < nblk) stage(i + 1, std::integral_constant<int, 1>{});
     }
 
     __bf16* obase = reinterpret_cast<__bf16*>(a.o) + bb * a.o_sb + hh * a.o_sh;
