@@ -376,15 +376,20 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
 
     const int32_t bb = bh / a.heads;
     const int32_t hh = bh - bb * a.heads;
-    __bf16* dkrow = reinterpret_cast<__bf16*>(g.dk) + bb * a.k_sb + hh * a.k_sh + (int64_t)ri.qseq * a.k_sr;
-    __bf16* dvrow = reinterpret_cast<__bf16*>(g.dv) + bb * a.v_sb + hh * a.v_sh + (int64_t)ri.qseq * a.v_sr;
+    // output rows (formed where they are written, not held across the loop)
+    auto dkrow = [&]() {
+        return reinterpret_cast<__bf16*>(g.dk) + bb * a.k_sb + hh * a.k_sh + (int64_t)ri.qseq * a.k_sr;
+    };
+    auto dvrow = [&]() {
+        return reinterpret_cast<__bf16*>(g.dv) + bb * a.v_sb + hh * a.v_sh + (int64_t)ri.qseq * a.v_sr;
+    };
     if (PAD && !dense && !__syncthreads_or(ri.store && !ri.pad)) {
         f32x16 zero[D / 32];
 #pragma unroll
         for (int dt = 0; dt < D / 32; ++dt) zero[dt] = f32x16{};
         if (ri.store) {
-            store_grad<D>(dkrow, zero, 0.f, h);
-            store_grad<D>(dvrow, zero, 0.f, h);
+            store_grad<D>(dkrow(), zero, 0.f, h);
+            store_grad<D>(dvrow(), zero, 0.f, h);
         }
         return;
     }
@@ -404,14 +409,6 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
     const int32_t qrow_b = (int32_t)(a.q_sr * 2), drow_b = (int32_t)(a.o_sr * 2);
     const float* lse2_bh = g.lse2 + (int64_t)bh * a.n_tot;
     const float* dlt_bh = g.delta + (int64_t)bh * a.n_tot;
-    int32_t srow[IPW], colk[IPW], colv[IPW];
-#pragma unroll
-    for (int j = 0; j < IPW; ++j) {
-        const int p = (wave * IPW + j) * 64 + lane;
-        srow[j] = p / G::CPR;
-        colk[j] = ((p % G::CPR) ^ G::fk(srow[j])) * 16;
-        colv[j] = ((p % G::CPR) ^ G::fv(srow[j])) * 16;
-    }
     const uint32_t q0 = lds_addr(&sm.q[0][wave * IPW * 1024]);
     const uint32_t qt0 = lds_addr(&sm.qt[0][wave * IPW * 1024]);
     const uint32_t d0 = lds_addr(&sm.d[0][wave * IPW * 1024]);
@@ -447,6 +444,18 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
             nd = dlt_bh[seq];
         }
         const uint32_t off = buf * SB;
+        // row and swizzled chunks of this lane's piece of load j, formed per
+        // stage (cheaper than holding them across the loop)
+        int lane_s = lane;
+        asm volatile("" : "+v"(lane_s));
+        int32_t srow[IPW], colk[IPW], colv[IPW];
+#pragma unroll
+        for (int j = 0; j < IPW; ++j) {
+            const int p = (wave * IPW + j) * 64 + lane_s;
+            srow[j] = p / G::CPR;
+            colk[j] = ((p % G::CPR) ^ G::fk(srow[j])) * 16;
+            colv[j] = ((p % G::CPR) ^ G::fv(srow[j])) * 16;
+        }
 #pragma unroll
         for (int j = 0; j < IPW; ++j) {
             int32_t qs;
@@ -488,12 +497,15 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
         if (!PAD || sm.slow[buf] != 2) {
             const uint8_t* qb = sm.q[buf];
             const uint8_t* db = sm.d[buf];
+            // lane bases recomputed per stage rather than held across the loop
+            int ka_s = ka, va_s = va;
+            asm volatile("" : "+v"(ka_s), "+v"(va_s));
             // S = Q K^T and dP = dO V^T: register e holds query
             // 8 (e/4) + 4 h + e%4 against this lane's key
             f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
             for (int kc = 0; kc < D / 16; ++kc) {
-                const int ad = ka ^ (32 * kc);
+                const int ad = ka_s ^ (32 * kc);
                 s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(qb + ad), kr[kc], s, 0, 0, 0);
                 dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(db + ad), vr[kc], dp, 0, 0,
                                                              0);
@@ -527,9 +539,9 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
             for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
                 for (int dt = 0; dt < D / 32; ++dt) {
-                    accv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(dtb, va, cc, dt), pb[cc],
+                    accv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(dtb, va_s, cc, dt), pb[cc],
                                                                        accv[dt], 0, 0, 0);
-                    acck[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(qtb, va, cc, dt), ds[cc],
+                    acck[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(qtb, va_s, cc, dt), ds[cc],
                                                                        acck[dt], 0, 0, 0);
                 }
         }
@@ -546,8 +558,8 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
         return;
     }
     if (!ri.store) return;
-    store_grad<D>(dkrow, acck, ri.pad ? 0.f : a.scale_log2 * 0.69314718055994530942f, h);
-    store_grad<D>(dvrow, accv, ri.pad ? 0.f : 1.f, h);
+    store_grad<D>(dkrow(), acck, ri.pad ? 0.f : a.scale_log2 * 0.69314718055994530942f, h);
+    store_grad<D>(dvrow(), accv, ri.pad ? 0.f : 1.f, h);
 }
 
 template <int D>
