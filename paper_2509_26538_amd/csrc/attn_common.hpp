@@ -93,10 +93,18 @@ __device__ __forceinline__ int32_t shared_seq(const Spans& sp, int32_t u) {
     return sp.map[u];  // u < cum[n] <= kMaxShared
 }
 
+// The runs are ascending and disjoint (the table's contract), so the one
+// that could hold seq is the last run starting at or before it: a binary
+// search over the starts.
 __device__ __forceinline__ bool is_shared_seq(const Spans& sp, int32_t seq) {
-    bool r = false;
-    for (int32_t s = 0; s < sp.n; ++s) r |= (seq >= sp.start[s]) & (seq < sp.start[s] + sp.len[s]);
-    return r;
+    int32_t lo = 0, hi = sp.n - 1;
+    if (hi < 0 || seq < sp.start[0]) return false;
+    while (lo < hi) {
+        const int32_t mid = (lo + hi + 1) >> 1;
+        if (sp.start[mid] <= seq) lo = mid;
+        else hi = mid - 1;
+    }
+    return seq < sp.start[lo] + sp.len[lo];
 }
 
 // Combine the two lane halves (lanes l and l^32 hold the same query row).
@@ -222,10 +230,15 @@ __device__ __forceinline__ int32_t load_spans(const AttnArgs& a, Spans& sp, int 
             sp.n = n_sp;
         }
         __syncthreads();
+        // token u belongs to the last run whose prefix count is <= u
         for (int u = tid; u < sp.cum[n_sp]; u += NT) {
-            int32_t s = 0;
-            while (s + 1 < n_sp && u >= sp.cum[s + 1]) ++s;
-            sp.map[u] = sp.start[s] + (u - sp.cum[s]);
+            int32_t lo = 0, hi = n_sp - 1;
+            while (lo < hi) {
+                const int32_t mid = (lo + hi + 1) >> 1;
+                if (sp.cum[mid] <= u) lo = mid;
+                else hi = mid - 1;
+            }
+            sp.map[u] = sp.start[lo] + (u - sp.cum[lo]);
         }
         const int32_t o_raw = a.sched[5];
         o = ((o_raw % a.n_img) + a.n_img) % a.n_img;

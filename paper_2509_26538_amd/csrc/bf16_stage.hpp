@@ -107,7 +107,9 @@ __device__ __forceinline__ ItemList item_list(const AttnArgs& a, bool dense, int
             bool keep = false;
             if (u < n_shared) {
                 seq = sp.map[u];
-                const int32_t rel = (seq - a.n_txt - r_start + a.n_img) % a.n_img;
+                // seq - n_txt and r_start lie in [0, n_img)
+                int32_t rel = seq - a.n_txt - r_start;
+                rel += rel < 0 ? a.n_img : 0;
                 keep = rel >= r_len;
             }
             const uint64_t bal = __builtin_amdgcn_ballot_w64(keep);
