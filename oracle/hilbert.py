@@ -31,16 +31,18 @@ Two constructions are given, and the tests require them to agree:
 import numpy as np
 
 
-def xy_iterative(order):
+def xy_iterative(order, d=None):
     """Return int64 arrays (x, y), indexed by Hilbert position d.
 
-    Vectorised over d; the loop runs over the ``order`` base-4 digits.
+    Vectorised over d (all positions of the order by default, or the given
+    ones); the loop runs over the ``order`` base-4 digits.
     """
     side = 1 << order
-    n = side * side
-    d = np.arange(n, dtype=np.int64)
-    x = np.zeros(n, dtype=np.int64)
-    y = np.zeros(n, dtype=np.int64)
+    if d is None:
+        d = np.arange(side * side, dtype=np.int64)
+    d = np.asarray(d, dtype=np.int64)
+    x = np.zeros(d.shape, dtype=np.int64)
+    y = np.zeros(d.shape, dtype=np.int64)
     t = d.copy()
     s = 1
     while s < side:

@@ -136,3 +136,13 @@ def test_curve_is_the_unique_self_similar_path(order):
 def test_rejects_grids_without_a_hilbert_curve(shape):
     with pytest.raises(ValueError):
         hilbert.build_perm(*shape)
+
+
+def test_decoding_chosen_positions_matches_the_full_decoding():
+    # the sampled form the largest-grid GPU test uses: positions given
+    # explicitly decode as they do in the full array
+    order = 7
+    x, y = hilbert.xy_iterative(order)
+    d = np.random.default_rng(3).integers(0, 1 << (2 * order), 500)
+    xs, ys = hilbert.xy_iterative(order, d)
+    assert np.array_equal(xs, x[d]) and np.array_equal(ys, y[d])
