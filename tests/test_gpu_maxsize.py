@@ -72,3 +72,51 @@ def test_gather_scatter_past_4gib(gpu):
     assert torch.equal(back, x)
     del x, y, back
     torch.cuda.empty_cache()
+
+
+def test_schedule_largest_grid(gpu):
+    # 32768 x 32768 in place, 16 tiles, an odd slide, an off-square shared
+    # region: the header and tiles against their closed forms (tile q covers
+    # the positions p with (p + o) mod N in [q N_T, (q + 1) N_T), so it starts
+    # at (q N_T - o) mod N), and the shared runs by what fixes them: every
+    # position of every run decodes (oracle bit-pair decoding) to a cell of
+    # the region, the runs are ascending, disjoint and maximal (the positions
+    # just outside decode outside the region) and cover its 32 x 31 cells.
+    side, n_txt, sh_h, sh_w, layer = 32768, 512, 32, 31, 5  # the largest regions hold 1024 tokens
+    n = side * side
+    tile, delta = n // 16, (1 << 24) + 12345
+    cfg = hb.hilberta_config(side, side, n_txt, tile, delta, sh_h, sh_w)
+    words = hb.hilberta_schedule_words(cfg)
+    sched = torch.full((words,), -77, dtype=torch.int32, device=gpu)
+    hb.hilberta_schedule(cfg, layer, sched)
+    torch.cuda.synchronize()
+    t = sched.cpu().numpy().astype(np.int64)
+    o = (layer * delta) % n
+    cap = sh_h + sh_w + 1
+    assert list(t[:12]) == [0x48424131, n_txt, n, tile, 16, o, t[6], sh_h * sh_w, layer, side, side, cap]
+    n_runs = int(t[6])
+    assert 1 <= n_runs <= cap
+    runs = t[12 + 64:12 + 64 + 2 * cap].reshape(cap, 2)
+    assert np.all(runs[n_runs:] == 0)
+    runs = runs[:n_runs]
+    starts, lens = runs[:, 0] - n_txt, runs[:, 1]
+    assert np.all(lens > 0) and np.all(starts[1:] > starts[:-1] + lens[:-1])  # ascending, disjoint, apart
+    assert int(lens.sum()) == sh_h * sh_w
+    r0, c0 = (side - sh_h) // 2, (side - sh_w) // 2
+
+    def inside(d):
+        x, y = hilbert.xy_iterative(15, d)
+        return (y >= r0) & (y < r0 + sh_h) & (x >= c0) & (x < c0 + sh_w)
+
+    pos = np.concatenate([s + np.arange(ln) for s, ln in zip(starts, lens)])
+    assert np.all(inside(pos))
+    before = starts - 1
+    after = starts + lens
+    assert not np.any(inside(before[before >= 0])) and not np.any(inside(after[after < n]))
+    for q in range(16):
+        start = (q * tile - o) % n
+        len1 = min(tile, n - start)
+        len2 = tile - len1
+        ns = sum(max(0, min(s + ln, e) - max(s, b)) for s, ln in zip(starts, lens)
+                 for b, e in ((start, start + len1), (0, len2)))
+        assert list(t[12 + 4 * q:16 + 4 * q]) == [n_txt + start, len1, len2, ns], q

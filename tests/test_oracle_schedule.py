@@ -219,3 +219,18 @@ def test_slide_direction_at_a_quarter_tile(g):
         if layer % 2:
             forward = ((p - o) % n) // nt
             assert not np.array_equal(same, forward[:, None] == forward[None, :])
+
+
+@pytest.mark.parametrize("layout,layer", [
+    (Layout(16, 16, 0, 64, 32, 4, 4), 3),
+    (Layout(32, 32, 77, 64, 48, 7, 5), 11),
+    (Layout(8, 8, 3, 16, 5, 3, 2), 7),
+    (Layout(64, 64, 512, 1024, 256, 16, 16), 2),
+])
+def test_scanned_tiles_match_the_closed_form(layout, layer):
+    # the closed form the largest-grid GPU test checks against: tile q starts
+    # at (q N_T - o) mod N and wraps after N - start positions
+    n, o = layout.tiled, schedule.offset(layout, layer)
+    for q, (start, len1, len2, _) in enumerate(schedule.tiles(layout, layer)):
+        s = (q * layout.tile - o) % n
+        assert (start, len1, len2) == (s, min(layout.tile, n - s), layout.tile - min(layout.tile, n - s))
