@@ -261,8 +261,10 @@ int hilberta_attn_bwd_workspace_bytes(const hilberta_config* cfg, int64_t batch,
  *              device tensors as for hilberta_attn_fwd; dq, dk, dv are
  *              written completely and may not overlap the inputs.
  *   lse        the forward's natural-log LSE, device float[batch*heads*N_tot].
- *   dtype      HILBERTA_BF16 only: bf16 tensors, fp32 accumulation, P and dS
- *              rounded to bf16 as matrix operands.
+ *   dtype      HILBERTA_BF16: bf16 tensors, fp32 accumulation, P and dS
+ *              rounded to bf16 as matrix operands.  HILBERTA_F32: fp32
+ *              tensors and fp32 arithmetic throughout (for exactness at
+ *              small sizes, not speed).
  *   scale      the forward's softmax scale.
  *   workspace  device scratch of at least hilberta_attn_bwd_workspace_bytes
  *              (required), 16-byte aligned.

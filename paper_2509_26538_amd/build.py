@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libhilberta.so")
-SOURCES = ["abi.cpp", "hilbert.hip", "permute.hip", "attn.hip", "attn_bf16.hip", "attn_bwd.hip"]
+SOURCES = ["abi.cpp", "hilbert.hip", "permute.hip", "attn.hip", "attn_bf16.hip", "attn_bwd.hip", "attn_bwd_f32.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -358,11 +358,12 @@ int run_attention_bwd(bool sparse, const hilberta_config* cfg, const int32_t* sc
     int rc = check_workspace(ws, ws_bytes);
     if (rc) return rc;
     if (dtype != HILBERTA_BF16 && dtype != HILBERTA_F32) return fail(HILBERTA_EUNSUPPORTED, "dtype %d", dtype);
-    if (dtype != HILBERTA_BF16) return fail(HILBERTA_EUNSUPPORTED, "the backward runs in bf16 only");
     Plan p{};
     hilberta::AttnArgs a{};
     bool empty = false;
-    rc = attn_setup(sparse, cfg, sched, t, 8, batch, heads, n_tot, head_dim, dtype, scale, true, p, a, empty);
+    // the fp32 kernels take every dense row whole (no key chunks)
+    rc = attn_setup(sparse, cfg, sched, t, 8, batch, heads, n_tot, head_dim, dtype, scale, dtype == HILBERTA_BF16,
+                    p, a, empty);
     if (rc || empty) return rc;
     if (!lse) return fail(HILBERTA_EINVAL, "lse is NULL");
     const int64_t need = bwd_ws_bytes(p, batch * heads, n_tot, head_dim);
@@ -379,7 +380,9 @@ int run_attention_bwd(bool sparse, const hilberta_config* cfg, const int32_t* sc
     g.delta = static_cast<float*>(ws);
     g.lse2 = static_cast<float*>(ws) + batch * heads * n_tot;
     a.ws = static_cast<float*>(ws) + bwd_rows_bytes(batch * heads, n_tot) / 4;  // 16-byte aligned
-    return hip_status(hilberta::launch_attn_bwd(a, g, (int)head_dim, static_cast<hipStream_t>(stream)),
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    return hip_status(dtype == HILBERTA_BF16 ? hilberta::launch_attn_bwd(a, g, (int)head_dim, st)
+                                             : hilberta::launch_attn_bwd_f32(a, g, (int)head_dim, st),
                       "backward launch");
 }
 
@@ -389,14 +392,15 @@ int bwd_ws_query(bool sparse, const hilberta_config* cfg, int64_t batch, int64_t
     if (batch < 0 || heads < 0 || n_tot < 0) return fail(HILBERTA_EINVAL, "negative size");
     if (head_dim != 64 && head_dim != 128)
         return fail(HILBERTA_EUNSUPPORTED, "head_dim %lld not in {64, 128}", (long long)head_dim);
-    if (dtype != HILBERTA_BF16) return fail(HILBERTA_EUNSUPPORTED, "the backward runs in bf16 only");
+    if (dtype != HILBERTA_BF16 && dtype != HILBERTA_F32) return fail(HILBERTA_EUNSUPPORTED, "dtype %d", dtype);
+    const bool split = dtype == HILBERTA_BF16;
     Plan p{};
     if (sparse) {
         const Geom g = geom(cfg);
         p = make_plan(true, g.prefix, g.tiled, g.shared_in_span, cfg->tile, n_tot, batch * heads, head_dim, dtype,
-                      true);
+                      split);
     } else {
-        p = make_plan(false, 0, n_tot, 0, n_tot, n_tot, batch * heads, head_dim, dtype, true);
+        p = make_plan(false, 0, n_tot, 0, n_tot, n_tot, batch * heads, head_dim, dtype, split);
     }
     *bytes = bwd_ws_bytes(p, batch * heads, n_tot, head_dim);
     return HILBERTA_OK;

@@ -95,6 +95,7 @@ struct BwdArgs {
     float* lse2;        // workspace: LSE in log2 units (0 for empty rows)
 };
 hipError_t launch_attn_bwd(const AttnArgs& a, const BwdArgs& g, int head_dim, hipStream_t s);
+hipError_t launch_attn_bwd_f32(const AttnArgs& a, const BwdArgs& g, int head_dim, hipStream_t s);
 
 // ----------------------------------------------------- permutation, schedule
 // perm[d] for the side x side curve positions: the raster index of the

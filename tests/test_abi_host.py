@@ -205,8 +205,8 @@ def _bwd(lib, cfg=None, dtype=hb.HILBERTA_BF16, lse=FAKE, ws=FAKE, wsb=1 << 30, 
 
 def test_backward_argument_errors(lib):
     # every call fails validation before any launch
-    assert _bwd(lib, dtype=hb.HILBERTA_F32) == hb.HILBERTA_EUNSUPPORTED
-    assert "bf16" in hb.last_error()
+    assert _bwd(lib, dtype=7) == hb.HILBERTA_EUNSUPPORTED
+    assert "dtype" in hb.last_error()
     assert _bwd(lib, lse=None) == hb.HILBERTA_EINVAL
     assert _bwd(lib, ws=None, wsb=0) == hb.HILBERTA_EINVAL
     assert _bwd(lib, wsb=100) == hb.HILBERTA_ECAPACITY
@@ -216,5 +216,9 @@ def test_backward_argument_errors(lib):
     assert hb.hilberta_attn_bwd_workspace_bytes(hb.make_config(16, 0, 64, 32, 4), 1, 2, 64,
                                                 hb.HILBERTA_BF16) == 2 * 256 * 8
     assert hb.dense_attn_bwd_workspace_bytes(2, 3, 100, 128, hb.HILBERTA_BF16) == 6 * 100 * 8
+    # fp32: dense rows are never split, so only the per-row words
+    assert hb.dense_attn_bwd_workspace_bytes(2, 3, 100, 128, hb.HILBERTA_F32) == 6 * 100 * 8
+    assert hb.hilberta_attn_bwd_workspace_bytes(hb.make_config(128, 512, 1024, 512, 16), 1, 24, 128,
+                                                hb.HILBERTA_F32) == 24 * 16896 * 8
     with pytest.raises(hb.HilbertaError):
-        hb.dense_attn_bwd_workspace_bytes(2, 3, 100, 128, hb.HILBERTA_F32)
+        hb.dense_attn_bwd_workspace_bytes(2, 3, 100, 128, 7)
