@@ -2,7 +2,8 @@
 powers of two and general shapes), text lengths, shared regions, both
 layouts, tile sizes among the divisors of the tiled span, slides and layers
 drawn at random.  Every row of the forward (fp32 and bf16) and of the
-backward (bf16) is compared, with the bounds of the other parity tests."""
+backward (fp32 and bf16) is compared, with the bounds of the other parity
+tests."""
 
 import numpy as np
 import pytest
@@ -14,6 +15,8 @@ from paper_2509_26538_amd import synth
 
 from attn_util import assert_close, assert_lse_close, hip_sparse, oracle_sparse
 from test_gpu_backward import assert_grads, run_sparse
+from test_gpu_backward_f32 import assert_grads as assert_grads_f32
+from test_gpu_backward_f32 import run_sparse as run_sparse_f32
 
 pytestmark = pytest.mark.gpu
 
@@ -63,6 +66,12 @@ def test_random_config(gpu, seed, layout):
         ro, rl = oracle_sparse(layout, layer, q, k, v)
         assert_close(o, ro, "f32", "fp32 layer %d" % layer)
         assert_lse_close(lse, rl, 1e-5)
+    g32 = torch.Generator(device="cpu").manual_seed(seed + 11)
+    do32 = torch.randn(q.shape, generator=g32)
+    got = run_sparse_f32(layout, layers[1], q, k, v, do32, gpu)
+    ref = gradients.masked_attention_grads(*(t.double().numpy() for t in (q, k, v, do32)),
+                                           lambda rows: schedule.mask_rows(layout, layers[1], rows))
+    assert_grads_f32(got, ref, "fp32 backward layer %d" % layers[1])
     qb, kb, vb = (t.to(torch.bfloat16) for t in (q, k, v))
     g = torch.Generator(device="cpu").manual_seed(seed + 7)
     do = torch.randn(qb.shape, generator=g).to(torch.bfloat16)
