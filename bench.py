@@ -42,7 +42,7 @@ N_LAYERS = 57              # Flux.1-dev: 19 double-stream + 38 single-stream blo
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hilberta_attn_fwd_flux128_traffic.json")
 # sources that decide the attention launch's kernels and work plan; counters
 # taken on an older build of them are not reported
-ATTN_SOURCES = ("attn_bf16.hip", "attn_common.hpp", "internal.hpp", "attn.hip", "abi.cpp")
+ATTN_SOURCES = ("attn_bf16.hip", "bf16_stage.hpp", "attn_common.hpp", "curve.hpp", "internal.hpp", "attn.hip", "abi.cpp")
 
 
 def attn_source_digest():
