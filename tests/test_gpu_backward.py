@@ -159,7 +159,7 @@ def sampled_keys(layout, layer, rng, n_tile_keys, n_global):
     return np.array(sorted(keys), dtype=np.int64)
 
 
-@pytest.mark.parametrize("name,n_global", [("flux-64", 2), ("flux-128", 0)])
+@pytest.mark.parametrize("name,n_global", [("flux-64", 2), ("flux-128", 0), ("stress-256", 0)])
 def test_fullsize_sampled_rows(gpu, name, n_global):
     # the benchmark's shapes (bf16, 24 heads, D 128): every gradient element
     # finite, and sampled rows of three heads against the oracle
