@@ -82,6 +82,36 @@ def test_sharp_softmax_bf16(gpu):
         assert_close(o, ro, "bf16", "layer %d" % layer, max_abs=2e-2)
 
 
+@pytest.mark.parametrize("order", ["rising", "falling"])
+def test_logit_scale_drifting_along_the_keys_bf16(gpu, order):
+    # Key norms ramp 16-fold along the sequence, so that the largest logits
+    # of a row (up to ~50 in log2 units) sit at the far end of its key list
+    # (rising: the running reference of the online softmax has to move up
+    # several times, by far more than any rescaling threshold) or at its
+    # start (falling: later keys add almost nothing).  The rows are sharp and
+    # |O| reaches ~4.1: the bf16 output rounding alone may then cost half an
+    # ulp (2^-6 = 1.6e-2 above 4), and the bf16 rounding of the dominant
+    # probabilities up to 2^-8 |O| more, so the max-abs bound is 3e-2
+    # (mean-abs stays 1e-3).
+    layout = Layout(32, 32, 40, 128, 64, 6, 6)
+    q, k, v = inputs(layout, 1, 2, 128, "bf16", seed=19)
+    ramp = torch.linspace(0.5, 8.0, layout.n_tot, dtype=torch.float32)
+    if order == "falling":
+        ramp = ramp.flip(0)
+    k = (k.float() * ramp[None, None, :, None]).to(torch.bfloat16)
+    for layer in (0, 1):
+        for split in (False, True):
+            o, lse = hip_sparse(layout, layer, q, k, v, gpu, split=split)
+            ro, rl = oracle_sparse(layout, layer, q, k, v)
+            what = "%s layer %d split %s" % (order, layer, split)
+            assert_close(o, ro, "bf16", what, max_abs=3e-2)
+            assert np.abs(lse - rl).max() <= 1e-3, what
+    od, dl = hip_dense(q, k, v, gpu)
+    ro, rl = oracle_rows(None, 0, q, k, v, np.arange(layout.n_tot))
+    assert_close(od, ro, "bf16", order + " dense", max_abs=3e-2)
+    assert np.abs(dl - rl).max() <= 1e-3
+
+
 def test_one_tile_equals_dense(gpu):
     # §3.2 with N_T = N_img: a single tile is dense attention
     layout = Layout(32, 32, 21, 1024, 256, 6, 6)
