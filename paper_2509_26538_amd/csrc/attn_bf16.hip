@@ -17,8 +17,9 @@
 // Staging.  K and V rows go straight from global memory into LDS with
 // bounds-checked buffer_load ... lds (no staging registers), double
 // buffered: stage i+1 is requested when stage i starts.  Rows are stored
-// unpadded with their 16-byte chunks XOR-swizzled by row: K chunk c of row r
-// sits at c ^ (r mod 16), so the 16 lanes that read one 16-byte piece of 16
+// unpadded with their 16-byte chunks XOR-swizzled by row (D = 128): K chunk
+// c of row r sits at c ^ (4 (r mod 4) + (r / 4 mod 4)), a bijection on any 16
+// consecutive rows, so the 16 lanes that read one 16-byte piece of 16
 // consecutive rows hit 16 different bank groups; V chunk c sits at
 // c ^ 4 (r mod 4), so the four rows that a transposing read touches at once
 // use disjoint 64-byte quarters of the banks.

@@ -20,9 +20,10 @@
 // No atomics: every gradient row is written once by the item that owns it,
 // so the results are deterministic.  Rows that attend every key (text and
 // shared rows) and keys every query attends are items of their own over the
-// whole sequence.  Each stage tensor is staged through LDS by direct loads
-// in the layout its reads need (fk for whole-row A operands, fv for the
-// transposing reads; Q, dO and K are read both ways and staged twice).
+// whole sequence.  Each stage tensor is staged once through LDS by direct
+// loads, in the fk layout, whose swizzle keeps both its whole-row reads (A
+// operands) and its transposing reads (Q, dO and K are read both ways)
+// free of bank conflicts.
 // Stages hold 32 list rows, so that the double-buffered stages of two
 // workgroups fit a CU's LDS and each SIMD interleaves two wavefronts.
 #include "bf16_stage.hpp"
@@ -147,8 +148,7 @@ constexpr int kBQ = 32;  // list rows per stage
 template <int D>
 struct SmemDq {
     static constexpr int SB = kBQ * Geo<D>::ROWB;
-    alignas(16) uint8_t k[2][SB];   // fk: A operand of S^T
-    alignas(16) uint8_t kt[2][SB];  // fv: transposed A operand of dQ^T
+    alignas(16) uint8_t k[2][SB];   // fk: A operand of S^T, transposed A operand of dQ^T
     alignas(16) uint8_t v[2][SB];   // fk: A operand of dP^T
     alignas(16) int32_t info[2][kBQ];
     Spans sp;
@@ -221,7 +221,6 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
         colv[j] = ((p % G::CPR) ^ G::fv(srow[j])) * 16;
     }
     const uint32_t k0 = lds_addr(&sm.k[0][wave * IPW * 1024]);
-    const uint32_t kt0 = lds_addr(&sm.kt[0][wave * IPW * 1024]);
     const uint32_t v0l = lds_addr(&sm.v[0][wave * IPW * 1024]);
 
     auto stage_fast = [&](int32_t i) -> bool {
@@ -259,7 +258,6 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
                 key = base >= 0 ? base + rr : list_seq(v0 + rr, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
             }
             dma16(krs, k0 + off + j * 1024, key * krow_b + colk[j]);
-            dma16(krs, kt0 + off + j * 1024, key * krow_b + colv[j]);
             dma16(vrs, v0l + off + j * 1024, key * vrow_b + colk[j]);
         }
         if (!PAD && !stage_fast(i) && tid < kBQ) {
@@ -270,7 +268,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
     };
 
     const int ka = row_base<D>(lane);
-    const int va = tr_base<D>(lane);
+    const int va0 = tr_base<D>(lane, 0), va1 = tr_base<D>(lane, 1);
     f32x16 acc[D / 32];
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt) acc[dt] = f32x16{};
@@ -312,13 +310,13 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
                     const float pe = __builtin_amdgcn_exp2f(fmaf(s[e], c, -lse2));
                     ds[cc][j] = (__bf16)(pe * (dp[e] - dlt));
                 }
-            const uint8_t* ktb = sm.kt[buf];
+            const uint8_t* ktb = sm.k[buf];
 #pragma unroll
             for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
                 for (int dt = 0; dt < D / 32; ++dt)
-                    acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(ktb, va, cc, dt), ds[cc], acc[dt],
-                                                                      0, 0, 0);
+                    acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(ktb, va0, va1, cc, dt), ds[cc],
+                                                                      acc[dt], 0, 0, 0);
         }
         wait_vmcnt<0>();
         __syncthreads();
@@ -335,10 +333,8 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
 template <int D>
 struct SmemDkdv {
     static constexpr int SB = kBQ * Geo<D>::ROWB;
-    alignas(16) uint8_t q[2][SB];   // fk: A operand of S
-    alignas(16) uint8_t qt[2][SB];  // fv: transposed A operand of dK^T
-    alignas(16) uint8_t d[2][SB];   // fk: dO, A operand of dP
-    alignas(16) uint8_t dt[2][SB];  // fv: dO, transposed A operand of dV^T
+    alignas(16) uint8_t q[2][SB];   // fk: A operand of S, transposed A operand of dK^T
+    alignas(16) uint8_t d[2][SB];   // fk: dO, A operand of dP, transposed A operand of dV^T
     alignas(16) float lse2[2][kBQ];
     alignas(16) float dlt[2][kBQ];
     alignas(16) int32_t info[2][kBQ];
@@ -410,9 +406,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
     const float* lse2_bh = g.lse2 + (int64_t)bh * a.n_tot;
     const float* dlt_bh = g.delta + (int64_t)bh * a.n_tot;
     const uint32_t q0 = lds_addr(&sm.q[0][wave * IPW * 1024]);
-    const uint32_t qt0 = lds_addr(&sm.qt[0][wave * IPW * 1024]);
     const uint32_t d0 = lds_addr(&sm.d[0][wave * IPW * 1024]);
-    const uint32_t dt0 = lds_addr(&sm.dt[0][wave * IPW * 1024]);
 
     float nl = 0.f, nd = 0.f;
     auto stage_fast = [&](int32_t i) -> bool {
@@ -466,15 +460,13 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
                 qs = base >= 0 ? base + rr : list_seq(v0 + rr, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
             }
             dma16(qrs, q0 + off + j * 1024, qs * qrow_b + colk[j]);
-            dma16(qrs, qt0 + off + j * 1024, qs * qrow_b + colv[j]);
             dma16(drs, d0 + off + j * 1024, qs * drow_b + colk[j]);
-            dma16(drs, dt0 + off + j * 1024, qs * drow_b + colv[j]);
         }
         if (!PAD && !stage_fast(i) && tid < kBQ) sm.info[buf][tid] = entry_info<false>(a, L, v, seq, o, sm.sp);
     };
 
     const int ka = row_base<D>(lane);
-    const int va = tr_base<D>(lane);
+    const int va0 = tr_base<D>(lane, 0), va1 = tr_base<D>(lane, 1);
     f32x16 acck[D / 32], accv[D / 32];
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt) {
@@ -498,8 +490,8 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
             const uint8_t* qb = sm.q[buf];
             const uint8_t* db = sm.d[buf];
             // lane bases recomputed per stage rather than held across the loop
-            int ka_s = ka, va_s = va;
-            asm volatile("" : "+v"(ka_s), "+v"(va_s));
+            int ka_s = ka, va0_s = va0, va1_s = va1;
+            asm volatile("" : "+v"(ka_s), "+v"(va0_s), "+v"(va1_s));
             // S = Q K^T and dP = dO V^T: register e holds query
             // 8 (e/4) + 4 h + e%4 against this lane's key
             f32x16 s = f32x16{}, dp = f32x16{};
@@ -533,15 +525,15 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
                         ds[cc][4 * j4 + t] = (__bf16)(pe * (dp[e] - d4[t]));
                     }
                 }
-            const uint8_t* dtb = sm.dt[buf];
-            const uint8_t* qtb = sm.qt[buf];
+            const uint8_t* dtb = sm.d[buf];
+            const uint8_t* qtb = sm.q[buf];
 #pragma unroll
             for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
                 for (int dt = 0; dt < D / 32; ++dt) {
-                    accv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(dtb, va_s, cc, dt), pb[cc],
+                    accv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(dtb, va0_s, va1_s, cc, dt), pb[cc],
                                                                        accv[dt], 0, 0, 0);
-                    acck[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(qtb, va_s, cc, dt), ds[cc],
+                    acck[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(qtb, va0_s, va1_s, cc, dt), ds[cc],
                                                                        acck[dt], 0, 0, 0);
                 }
         }

@@ -4,11 +4,13 @@
 // work item.
 //
 // A stage holds 64 rows of D bf16 values, unpadded, each row's 16-byte
-// chunks XOR-swizzled by the row index: fk for rows read whole as an MFMA
-// A operand (16 consecutive rows read one chunk each hit 16 different bank
-// groups), fv for rows read with the transposing ds_read_b64_tr_b16 (the
-// four rows one transposing read touches use disjoint quarters of the
-// banks).
+// chunks XOR-swizzled by the row index.  fk serves rows read whole as an
+// MFMA A operand and rows read with the transposing ds_read_b64_tr_b16 alike,
+// so a tensor read both ways is staged once: it is a bijection on every 16
+// consecutive rows (16 lanes that read one chunk each of 16 consecutive rows
+// hit 16 different bank groups), and the four aligned consecutive rows that
+// one transposing read touches land in disjoint quarters of the banks.  fv
+// serves rows that are only read transposed (the forward's V).
 #pragma once
 
 #include "attn_common.hpp"
@@ -25,8 +27,14 @@ struct Geo {
     static constexpr int ROWB = D * 2;             // bytes per row
     static constexpr int STAGEB = kBN * ROWB;      // bytes per tensor and stage
     static constexpr int IPW = STAGEB / 1024 / 4;  // 1 KB direct loads per wavefront and tensor
-    // chunk swizzles (XOR on the 16-byte chunk index of a row)
-    __device__ __forceinline__ static int fk(int row) { return D == 128 ? (row & 15) : ((row >> 1) & 7); }
+    // chunk swizzles (XOR on the 16-byte chunk index of a row).  D = 128:
+    // a row spans all 64 banks and fk puts row bits 0-1 on the quarter (chunk
+    // bits 2-3), bits 2-3 on the chunk within it.  D = 64: two rows share the
+    // banks (row bit 0 picks the half), fk puts row bit 1 on the quarter
+    // within the half and bits 2-3 on the chunk within it.
+    __device__ __forceinline__ static int fk(int row) {
+        return D == 128 ? 4 * (row & 3) + ((row >> 2) & 3) : 4 * ((row >> 1) & 1) + ((row >> 2) & 3);
+    }
     __device__ __forceinline__ static int fv(int row) { return D == 128 ? 4 * (row & 3) : 4 * ((row >> 1) & 1); }
 };
 
@@ -144,36 +152,39 @@ __device__ __forceinline__ int32_t entry_info(const AttnArgs& a, const ItemList&
 }
 
 // A operand of 32 rows x 16 columns (bf16x8 per lane) taken transposed from
-// a stage in the fv layout: rows 16 cc .. 16 cc + 15 of the stage become the
+// a stage in the fk layout: rows 16 cc .. 16 cc + 15 of the stage become the
 // reduction index, in the order the score registers hold them (chunk cc of
 // 16 list entries: register j holds entry 16 cc + 8 (j/4) + 4 h + j%4), and
-// columns 32 dt .. 32 dt + 31 of the rows the 32 output rows.  va is the
-// lane's base address (see tr_base).
+// columns 32 dt .. 32 dt + 31 of the rows the 32 output rows.  The two reads
+// cover rows 8 rd + 4 h + jj/4 (rd = 0, 1), whose swizzles differ, so each
+// has its own lane base (tr_base); the column block dt flips only address
+// bits 6-7 (the chunk index is 4 dt + c0 with c0 < 4, and fk moves whole
+// quarters apart or chunks within one), and 16 rows further on is 16 ROWB
+// further on (fk looks at row bits 0-3 only).
 template <int D>
-__device__ __forceinline__ bf16x8 tr_operand(const uint8_t* buf, int va, int cc, int dt) {
-    const uint8_t* vp = buf + (va ^ (64 * dt)) + 16 * cc * Geo<D>::ROWB;
-    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vp));
-    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vp + 8 * Geo<D>::ROWB));
+__device__ __forceinline__ bf16x8 tr_operand(const uint8_t* buf, int va0, int va1, int cc, int dt) {
+    const int rows = 16 * cc * Geo<D>::ROWB;
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(buf + (va0 ^ (64 * dt)) + rows));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(buf + (va1 ^ (64 * dt)) + rows));
     return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
-// Lane base addresses in a stage: ka for whole-row reads of the fk layout
-// (row 32 kt + ql, chunk 2 kc + h: address (ka ^ 32 kc) + kt 32 ROWB), va
-// for the transposing reads of the fv layout (lane group gi = lane/16 and
-// jj = lane%16 read row 16 cc + 8 rd + 4 h + jj/4 at columns 32 dt +
-// 16 (gi%2) + 4 (jj%4)).
+template <int D>
+__device__ __forceinline__ int tr_base(int lane, int rd) {
+    const int h = lane >> 5, gi = lane >> 4, jj = lane & 15;
+    const int row = 8 * rd + 4 * h + (jj >> 2);
+    const int c0 = 2 * (gi & 1) + ((jj & 3) >> 1);
+    return row * Geo<D>::ROWB + ((c0 ^ Geo<D>::fk(row)) * 16) + ((jj & 3) & 1) * 8;
+}
+
+// Lane base address for whole-row reads of the fk layout: row 32 kt + ql,
+// chunk 2 kc + h at address (ka ^ 32 kc) + kt 32 ROWB.
 template <int D>
 __device__ __forceinline__ int row_base(int lane) {
     const int ql = lane & 31, h = lane >> 5;
     return ql * Geo<D>::ROWB + ((h ^ Geo<D>::fk(ql)) * 16);
 }
 
-template <int D>
-__device__ __forceinline__ int tr_base(int lane) {
-    const int h = lane >> 5, gi = lane >> 4, jj = lane & 15;
-    const int vrow = 4 * h + (jj >> 2);
-    return vrow * Geo<D>::ROWB + (((2 * (gi & 1) + ((jj & 3) >> 1)) ^ Geo<D>::fv(vrow)) * 16) + ((jj & 3) & 1) * 8;
-}
 
 }  // namespace
 }  // namespace hilberta
