@@ -212,13 +212,12 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
     // direct loads: lane l of load j fills LDS chunk p = (w IPW + j) 64 + l
     // of the stage, i.e. row p / CPR, stored chunk p % CPR, which holds
     // global chunk (p % CPR) ^ f(row)
-    int32_t srow[IPW], colk[IPW], colv[IPW];
+    int32_t srow[IPW], colk[IPW];
 #pragma unroll
     for (int j = 0; j < IPW; ++j) {
         const int p = (wave * IPW + j) * 64 + lane;
         srow[j] = p / G::CPR;
         colk[j] = ((p % G::CPR) ^ G::fk(srow[j])) * 16;
-        colv[j] = ((p % G::CPR) ^ G::fv(srow[j])) * 16;
     }
     const uint32_t k0 = lds_addr(&sm.k[0][wave * IPW * 1024]);
     const uint32_t v0l = lds_addr(&sm.v[0][wave * IPW * 1024]);
@@ -442,14 +441,13 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
         // stage (cheaper than holding them across the loop)
         int lane_s = lane;
         asm volatile("" : "+v"(lane_s));
-        int32_t srow[IPW], colk[IPW], colv[IPW];
+        int32_t srow[IPW], colk[IPW];
 #pragma unroll
         for (int j = 0; j < IPW; ++j) {
             const int p = (wave * IPW + j) * 64 + lane_s;
             srow[j] = p / G::CPR;
             colk[j] = ((p % G::CPR) ^ G::fk(srow[j])) * 16;
-            colv[j] = ((p % G::CPR) ^ G::fv(srow[j])) * 16;
-        }
+            }
 #pragma unroll
         for (int j = 0; j < IPW; ++j) {
             int32_t qs;
