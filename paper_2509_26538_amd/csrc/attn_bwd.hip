@@ -28,6 +28,8 @@
 // workgroups fit a CU's LDS and each SIMD interleaves two wavefronts.
 #include "bf16_stage.hpp"
 
+#include <type_traits>
+
 namespace hilberta {
 namespace {
 
@@ -277,8 +279,10 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
     load_stage(0, 0);
     wait_vmcnt<0>();
     __syncthreads();
-    for (int32_t i = 0; i < nblk; ++i) {
-        const int buf = i & 1;
+    // one stage; the buffer index is a compile-time constant (the loop
+    // below runs stages in pairs), so LDS addresses carry it as an immediate
+    auto stage = [&](int32_t i, auto buf_c) {
+        constexpr int buf = decltype(buf_c)::value;
         if (i + 1 < nblk) load_stage(i + 1, buf ^ 1);
         if (!PAD || sm.slow[buf] != 2) {
             const uint8_t* kb_ = sm.k[buf];
@@ -319,6 +323,10 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
         }
         wait_vmcnt<0>();
         __syncthreads();
+    };
+    for (int32_t i = 0; i < nblk; i += 2) {
+        stage(i, std::integral_constant<int, 0>{});
+        if (i + 1 < nblk) stage(i + 1, std::integral_constant<int, 1>{});
     }
     if (dense && a.n_chunks > 1) {
         store_partial<D>(a, bh, chunk, ri.dense_row, 0, acc, h);
@@ -481,8 +489,9 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
         sm.dlt[0][lane] = nd;
     }
     __syncthreads();
-    for (int32_t i = 0; i < nblk; ++i) {
-        const int buf = i & 1;
+    // one stage, the buffer index a compile-time constant as in the dQ pass
+    auto stage = [&](int32_t i, auto buf_c) {
+        constexpr int buf = decltype(buf_c)::value;
         if (i + 1 < nblk) load_stage(i + 1, buf ^ 1);
         if (!PAD || sm.slow[buf] != 2) {
             const uint8_t* qb = sm.q[buf];
@@ -541,6 +550,10 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
             sm.dlt[buf ^ 1][lane] = nd;
         }
         __syncthreads();
+    };
+    for (int32_t i = 0; i < nblk; i += 2) {
+        stage(i, std::integral_constant<int, 0>{});
+        if (i + 1 < nblk) stage(i + 1, std::integral_constant<int, 1>{});
     }
     if (dense && a.n_chunks > 1) {
         store_partial<D>(a, bh, chunk, ri.dense_row, 0, acck, h);
