@@ -205,6 +205,11 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
     }
     const float lse2 = g.lse2[(int64_t)bh * a.n_tot + ri.qseq];
     const float dlt = g.delta[(int64_t)bh * a.n_tot + ri.qseq];
+    // dP - Dlt comes out of the dP^T products: their accumulator starts at
+    // -Dlt of this lane's row
+    f32x16 ndlt16;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) ndlt16[e] = -dlt;
 
     const __bf16* kbase = reinterpret_cast<const __bf16*>(a.k) + bb * a.k_sb + hh * a.k_sh;
     const __bf16* vbase = reinterpret_cast<const __bf16*>(a.v) + bb * a.v_sb + hh * a.v_sh;
@@ -289,7 +294,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
             const uint8_t* vb_ = sm.v[buf];
             // S^T = K Q^T and dP^T = V dO^T: register e holds key
             // 8 (e/4) + 4 h + e%4 against this lane's row
-            f32x16 s = f32x16{}, dp = f32x16{};
+            f32x16 s = f32x16{}, dp = ndlt16;
 #pragma unroll
             for (int kc = 0; kc < D / 16; ++kc) {
                 const int ad = ka ^ (32 * kc);
@@ -311,7 +316,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
                 for (int j = 0; j < 8; ++j) {
                     const int e = 8 * cc + j;
                     const float pe = __builtin_amdgcn_exp2f(fmaf(s[e], c, -lse2));
-                    ds[cc][j] = (__bf16)(pe * (dp[e] - dlt));
+                    ds[cc][j] = (__bf16)(pe * dp[e]);
                 }
             const uint8_t* ktb = sm.k[buf];
 #pragma unroll
@@ -343,7 +348,7 @@ struct SmemDkdv {
     alignas(16) uint8_t q[2][SB];   // fk: A operand of S, transposed A operand of dK^T
     alignas(16) uint8_t d[2][SB];   // fk: dO, A operand of dP, transposed A operand of dV^T
     alignas(16) float lse2[2][kBQ];
-    alignas(16) float dlt[2][kBQ];
+    alignas(16) float ndlt[2][kBQ];  // -Dlt of the stage's queries
     alignas(16) int32_t info[2][kBQ];
     Spans sp;
     int32_t n_keep;
@@ -486,7 +491,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
     wait_vmcnt<0>();
     if (wave == 0 && lane < kBQ) {
         sm.lse2[0][lane] = nl;
-        sm.dlt[0][lane] = nd;
+        sm.ndlt[0][lane] = -nd;
     }
     __syncthreads();
     // one stage, the buffer index a compile-time constant as in the dQ pass
@@ -500,8 +505,16 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
             int ka_s = ka, va0_s = va0, va1_s = va1;
             asm volatile("" : "+v"(ka_s), "+v"(va0_s), "+v"(va1_s));
             // S = Q K^T and dP = dO V^T: register e holds query
-            // 8 (e/4) + 4 h + e%4 against this lane's key
-            f32x16 s = f32x16{}, dp = f32x16{};
+            // 8 (e/4) + 4 h + e%4 against this lane's key.  The dP
+            // accumulator starts at the queries' -Dlt, so dP - Dlt comes out
+            // of the products.
+            f32x16 s = f32x16{}, dp;
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4) {
+                const f4 d4 = *reinterpret_cast<const f4*>(&sm.ndlt[buf][8 * g4 + 4 * h]);
+#pragma unroll
+                for (int t = 0; t < 4; ++t) dp[4 * g4 + t] = d4[t];
+            }
 #pragma unroll
             for (int kc = 0; kc < D / 16; ++kc) {
                 const int ad = ka_s ^ (32 * kc);
@@ -523,13 +536,12 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
                 for (int j4 = 0; j4 < 2; ++j4) {
                     const int g4 = 2 * cc + j4;
                     const f4 l4 = *reinterpret_cast<const f4*>(&sm.lse2[buf][8 * g4 + 4 * h]);
-                    const f4 d4 = *reinterpret_cast<const f4*>(&sm.dlt[buf][8 * g4 + 4 * h]);
 #pragma unroll
                     for (int t = 0; t < 4; ++t) {
                         const int e = 4 * g4 + t;
                         const float pe = __builtin_amdgcn_exp2f(fmaf(s[e], c, -l4[t]));
                         pb[cc][4 * j4 + t] = (__bf16)pe;
-                        ds[cc][4 * j4 + t] = (__bf16)(pe * (dp[e] - d4[t]));
+                        ds[cc][4 * j4 + t] = (__bf16)(pe * dp[e]);
                     }
                 }
             const uint8_t* dtb = sm.d[buf];
@@ -547,7 +559,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
         wait_vmcnt<0>();
         if (wave == 0 && lane < kBQ && i + 1 < nblk) {
             sm.lse2[buf ^ 1][lane] = nl;
-            sm.dlt[buf ^ 1][lane] = nd;
+            sm.ndlt[buf ^ 1][lane] = -nd;
         }
         __syncthreads();
     };
