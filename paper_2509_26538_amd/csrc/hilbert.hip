@@ -92,37 +92,63 @@ __device__ int32_t shared_runs(RunsLds& r, int32_t side, int32_t grid_h, int32_t
     return n_runs;
 }
 
-// The schedule's header and shared runs (none in the moved-prefix layout,
-// where the shared tokens sit in the prefix).  One workgroup.
-__global__ void __launch_bounds__(256) shared_runs_kernel(ScheduleArgs a) {
+// The schedule in one launch.  Tiles of the slid partition: tile q holds
+// the positions p of the tiled span (N tokens) with
+// floor(((p + o) mod N) / N_T) = q, i.e. the cyclic range that starts at
+// (q N_T - o) mod N; each carries the count of shared tokens inside it.
+// Every workgroup finds the shared runs for itself (none in the moved-prefix
+// layout, where the shared tokens sit in the prefix) and writes its 256
+// tiles; workgroup 0 also writes the header and the runs.
+__global__ void __launch_bounds__(256) schedule_kernel(ScheduleArgs a) {
     __shared__ RunsLds r;
     const int tid = threadIdx.x;
     const int32_t n_cells = a.shared_h * a.shared_w;
-    const int32_t n_runs = a.moved || n_cells == 0 ? 0 : shared_runs(r, a.side, a.grid_h, a.grid_w, a.shared_h, a.shared_w, a.span_cap);
-    int32_t* spans = a.out + 12 + 4 * a.n_tiles;
-    for (int32_t i = tid; i < n_runs; i += blockDim.x) {
-        spans[2 * i] = a.prefix + r.sorted_starts[i];
-        spans[2 * i + 1] = r.sorted_ends[i] + 1 - r.sorted_starts[i];
+    const int32_t n_runs =
+        a.moved || n_cells == 0 ? 0 : shared_runs(r, a.side, a.grid_h, a.grid_w, a.shared_h, a.shared_w, a.span_cap);
+    if (blockIdx.x == 0) {
+        int32_t* spans = a.out + 12 + 4 * a.n_tiles;
+        for (int32_t i = tid; i < n_runs; i += blockDim.x) {
+            spans[2 * i] = a.prefix + r.sorted_starts[i];
+            spans[2 * i + 1] = r.sorted_ends[i] + 1 - r.sorted_starts[i];
+        }
+        for (int32_t i = n_runs + tid; i < a.span_cap; i += blockDim.x) {
+            spans[2 * i] = 0;
+            spans[2 * i + 1] = 0;
+        }
+        if (tid == 0) {
+            int32_t* h = a.out;
+            h[0] = 0x48424131;
+            h[1] = a.prefix;
+            h[2] = a.tiled;
+            h[3] = a.tile;
+            h[4] = a.n_tiles;
+            h[5] = a.offset;
+            h[6] = n_runs;
+            h[7] = n_cells;
+            h[8] = a.layer;
+            h[9] = a.grid_h;
+            h[10] = a.grid_w;
+            h[11] = a.span_cap;
+        }
     }
-    for (int32_t i = n_runs + tid; i < a.span_cap; i += blockDim.x) {
-        spans[2 * i] = 0;
-        spans[2 * i + 1] = 0;
+    const int32_t q = blockIdx.x * blockDim.x + tid;
+    if (q >= a.n_tiles) return;
+    const int32_t n_img = a.tiled;
+    const int32_t start = (int32_t)(((int64_t)q * a.tile - a.offset + n_img) % n_img);
+    const int32_t len1 = min(a.tile, n_img - start);
+    const int32_t len2 = a.tile - len1;
+    int32_t ns = 0;
+    for (int32_t s = 0; s < n_runs; ++s) {
+        const int32_t lo = r.sorted_starts[s];
+        const int32_t hi = r.sorted_ends[s] + 1;
+        ns += max(0, min(hi, start + len1) - max(lo, start));
+        ns += max(0, min(hi, len2) - max(lo, 0));
     }
-    if (tid == 0) {
-        int32_t* h = a.out;
-        h[0] = 0x48424131;
-        h[1] = a.prefix;
-        h[2] = a.tiled;
-        h[3] = a.tile;
-        h[4] = a.n_tiles;
-        h[5] = a.offset;
-        h[6] = n_runs;
-        h[7] = n_cells;
-        h[8] = a.layer;
-        h[9] = a.grid_h;
-        h[10] = a.grid_w;
-        h[11] = a.span_cap;
-    }
+    int32_t* t = a.out + 12 + 4 * q;
+    t[0] = a.prefix + start;
+    t[1] = len1;
+    t[2] = len2;
+    t[3] = ns;
 }
 
 // The moved-prefix order of the image tokens: the shared tokens first, then
@@ -155,33 +181,6 @@ __global__ void __launch_bounds__(256) build_perm_moved_kernel(int32_t side, int
     }
 }
 
-// Tiles of the slid partition: tile q holds the positions p of the tiled
-// span (N tokens) with floor(((p + o) mod N) / N_T) = q, i.e. the cyclic range
-// that starts at (q N_T - o) mod N.  Reads the runs written by
-// shared_runs_kernel to count the shared tokens inside each tile.
-__global__ void __launch_bounds__(256) tiles_kernel(ScheduleArgs a) {
-    const int32_t q = blockIdx.x * blockDim.x + threadIdx.x;
-    if (q >= a.n_tiles) return;
-    const int32_t n_img = a.tiled;
-    const int32_t start = (int32_t)(((int64_t)q * a.tile - a.offset + n_img) % n_img);
-    const int32_t len1 = min(a.tile, n_img - start);
-    const int32_t len2 = a.tile - len1;
-    const int32_t* spans = a.out + 12 + 4 * a.n_tiles;
-    const int32_t n_runs = a.out[6];
-    int32_t ns = 0;
-    for (int32_t s = 0; s < n_runs; ++s) {
-        const int32_t lo = spans[2 * s] - a.prefix;
-        const int32_t hi = lo + spans[2 * s + 1];
-        ns += max(0, min(hi, start + len1) - max(lo, start));
-        ns += max(0, min(hi, len2) - max(lo, 0));
-    }
-    int32_t* t = a.out + 12 + 4 * q;
-    t[0] = a.prefix + start;
-    t[1] = len1;
-    t[2] = len2;
-    t[3] = ns;
-}
-
 }  // namespace
 
 hipError_t launch_build_perm(int32_t side, int32_t grid_h, int32_t grid_w, int32_t* perm, int32_t* inv,
@@ -204,11 +203,8 @@ hipError_t launch_build_perm_moved(int32_t side, int32_t shared_h, int32_t share
 }
 
 hipError_t launch_schedule(const ScheduleArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(shared_runs_kernel, dim3(1), dim3(256), 0, s, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const int blocks = (a.n_tiles + 255) / 256;
-    hipLaunchKernelGGL(tiles_kernel, dim3(blocks), dim3(256), 0, s, a);
+    const int blocks = a.n_tiles > 256 ? (a.n_tiles + 255) / 256 : 1;
+    hipLaunchKernelGGL(schedule_kernel, dim3(blocks), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
