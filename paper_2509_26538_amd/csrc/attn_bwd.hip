@@ -24,8 +24,9 @@
 // loads, in the fk layout, whose swizzle keeps both its whole-row reads (A
 // operands) and its transposing reads (Q, dO and K are read both ways)
 // free of bank conflicts.
-// Stages hold 32 list rows, so that the double-buffered stages of two
-// workgroups fit a CU's LDS and each SIMD interleaves two wavefronts.
+// Stages hold 32 list rows, so that two workgroups fit a CU (64-row stages
+// would take 82 KB of LDS per workgroup and more than 256 registers per lane
+// in the dK/dV pass) and each SIMD interleaves two wavefronts.
 #include "bf16_stage.hpp"
 
 #include <type_traits>
