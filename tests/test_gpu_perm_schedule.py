@@ -42,6 +42,8 @@ LAYOUTS = [
     Layout(2, 2, 1, 1, 1, 1, 1),               # smallest grid, one-token tiles
     Layout(32, 32, 77, 64, 48, 7, 5),          # off-centre odd region, many runs
     Layout(16, 16, 0, 256, 0, 16, 16),         # the whole grid is shared
+    Layout(64, 64, 0, 8, 3, 8, 8),             # 512 tiles: more than one workgroup of tiles
+    Layout(128, 128, 7, 16, 5, 16, 16),        # 1024 tiles
 ]
 
 
