@@ -126,6 +126,23 @@ def test_sparse_backward(gpu, layout, head_dim):
                 assert np.all(g[:, :, pad] == 0)
 
 
+@pytest.mark.parametrize("order", ["rising", "falling"])
+def test_backward_with_logit_scale_drifting_along_the_keys(gpu, order):
+    # Key norms ramp 16-fold along the sequence (logits up to ~50 in log2
+    # units at one end), so rows are sharp and their probabilities span many
+    # binades; the gradients keep the same relative bounds.
+    layout = Layout(32, 32, 40, 128, 64, 6, 6)
+    q, k, v, do = inputs(layout.n_tot, 1, 2, 128, seed=23)
+    ramp = torch.linspace(0.5, 8.0, layout.n_tot, dtype=torch.float32)
+    if order == "falling":
+        ramp = ramp.flip(0)
+    k = (k.float() * ramp[None, None, :, None]).to(k.dtype)
+    for layer in (0, 1):
+        got = run_sparse(layout, layer, q, k, v, do, gpu)
+        ref = oracle(q, k, v, do, lambda rows: schedule.mask_rows(layout, layer, rows))
+        assert_grads(got, ref, "%s layer %d" % (order, layer))
+
+
 @pytest.mark.parametrize("n,head_dim", [(200, 64), (333, 128), (64, 128), (1100, 64)])
 def test_dense_backward(gpu, n, head_dim):
     q, k, v, do = inputs(n, 2, 2, head_dim, seed=n)
