@@ -65,14 +65,19 @@ __global__ void __launch_bounds__(256) bwd_prep_kernel(AttnArgs a, BwdArgs g) {
     }
 }
 
+// One lane's gradient row, scaled by mul; a padding slot (zero) is written
+// as zeros by selection, never as acc * 0: a padding row's sums may hold
+// inf or NaN (its probabilities are not masked, and the caller may fill the
+// slot with anything finite), and inf * 0 is NaN.
 template <int D>
-__device__ __forceinline__ void store_grad(__bf16* row, const f32x16 acc[D / 32], float mul, int h) {
+__device__ __forceinline__ void store_grad(__bf16* row, const f32x16 acc[D / 32], float mul, bool zero, int h) {
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-            store4<__bf16>(row + 32 * dt + 8 * q + 4 * h, acc[dt][4 * q] * mul, acc[dt][4 * q + 1] * mul,
-                           acc[dt][4 * q + 2] * mul, acc[dt][4 * q + 3] * mul);
+            store4<__bf16>(row + 32 * dt + 8 * q + 4 * h, zero ? 0.f : acc[dt][4 * q] * mul,
+                           zero ? 0.f : acc[dt][4 * q + 1] * mul, zero ? 0.f : acc[dt][4 * q + 2] * mul,
+                           zero ? 0.f : acc[dt][4 * q + 3] * mul);
 }
 
 // Rows that attend every key (dQ) and keys every query attends (dK, dV) are
@@ -193,7 +198,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
         f32x16 zero[D / 32];
 #pragma unroll
         for (int dt = 0; dt < D / 32; ++dt) zero[dt] = f32x16{};
-        if (ri.store) store_grad<D>(dqrow, zero, 0.f, h);
+        if (ri.store) store_grad<D>(dqrow, zero, 0.f, true, h);
         return;
     }
     const int64_t qoff = bb * a.q_sb + hh * a.q_sh + (int64_t)ri.qseq * a.q_sr;
@@ -339,7 +344,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
         return;
     }
     if (!ri.store) return;
-    store_grad<D>(dqrow, acc, ri.pad ? 0.f : a.scale_log2 * 0.69314718055994530942f, h);
+    store_grad<D>(dqrow, acc, a.scale_log2 * 0.69314718055994530942f, ri.pad, h);
 }
 
 // -------------------------------------------------------------------- dK dV
@@ -397,8 +402,8 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
 #pragma unroll
         for (int dt = 0; dt < D / 32; ++dt) zero[dt] = f32x16{};
         if (ri.store) {
-            store_grad<D>(dkrow(), zero, 0.f, h);
-            store_grad<D>(dvrow(), zero, 0.f, h);
+            store_grad<D>(dkrow(), zero, 0.f, true, h);
+            store_grad<D>(dvrow(), zero, 0.f, true, h);
         }
         return;
     }
@@ -574,8 +579,8 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
         return;
     }
     if (!ri.store) return;
-    store_grad<D>(dkrow(), acck, ri.pad ? 0.f : a.scale_log2 * 0.69314718055994530942f, h);
-    store_grad<D>(dvrow(), accv, ri.pad ? 0.f : 1.f, h);
+    store_grad<D>(dkrow(), acck, a.scale_log2 * 0.69314718055994530942f, ri.pad, h);
+    store_grad<D>(dvrow(), accv, 1.f, ri.pad, h);
 }
 
 template <int D>

@@ -114,10 +114,12 @@ __global__ void __launch_bounds__(kThreads) bwd_dq_f32_kernel(AttnArgs a, BwdArg
         for (int e = 0; e < H2; ++e) acc[e] = fmaf(ds, kr[e], acc[e]);
     }
     if (!ri.store) return;
-    const float mul = ri.pad ? 0.f : c * 0.69314718055994530942f;  // the softmax scale
+    const float mul = c * 0.69314718055994530942f;  // the softmax scale
     float* out = static_cast<float*>(g.dq) + it.bb * a.q_sb + it.hh * a.q_sh + (int64_t)ri.qseq * a.q_sr + half * H2;
+    // a padding slot is written as zeros by selection: its sums may be inf
+    // or NaN, and inf * 0 is NaN
 #pragma unroll
-    for (int e = 0; e < H2; ++e) out[e] = acc[e] * mul;
+    for (int e = 0; e < H2; ++e) out[e] = ri.pad ? 0.f : acc[e] * mul;
 }
 
 template <int D, bool PAD>
@@ -164,13 +166,13 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_f32_kernel(AttnArgs a, BwdA
         }
     }
     if (!ri.store) return;
-    const float mk = ri.pad ? 0.f : c * 0.69314718055994530942f, mv = ri.pad ? 0.f : 1.f;
+    const float mk = c * 0.69314718055994530942f;
     float* ok_ = static_cast<float*>(g.dk) + it.bb * a.k_sb + it.hh * a.k_sh + (int64_t)ri.qseq * a.k_sr + half * H2;
     float* ov = static_cast<float*>(g.dv) + it.bb * a.v_sb + it.hh * a.v_sh + (int64_t)ri.qseq * a.v_sr + half * H2;
 #pragma unroll
     for (int e = 0; e < H2; ++e) {
-        ok_[e] = ak[e] * mk;
-        ov[e] = av[e] * mv;
+        ok_[e] = ri.pad ? 0.f : ak[e] * mk;
+        ov[e] = ri.pad ? 0.f : av[e];
     }
 }
 

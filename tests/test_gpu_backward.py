@@ -228,3 +228,32 @@ def test_empty_batch_is_a_no_op(gpu):
     z = torch.empty(0, 2, layout.n_tot, 64, dtype=torch.bfloat16, device=gpu)
     lse = torch.empty(0, 2, layout.n_tot, dtype=torch.float32, device=gpu)
     hb.hilberta_attn_bwd(cfg, sched, z, z, z, z, z, lse, z, z, z, None)
+
+
+def fill_padding(layout, tensors, seed):
+    """Copies with large finite values (300 N(0,1)) in the padding slots."""
+    pad = layout.n_txt + np.nonzero(~schedule.valid_hilbert(layout))[0]
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    out = []
+    for t in tensors:
+        t = t.clone()
+        t[:, :, pad] = (300 * torch.randn(t[:, :, pad].shape, generator=g)).to(t.dtype)
+        out.append(t)
+    return pad, out
+
+
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_padding_slot_values_do_not_leak_into_gradients(gpu, head_dim):
+    # Appendix D: padding is masked as keys and as queries.  With large
+    # finite values in the padding slots of Q, K, V and dO, a padding row's
+    # unmasked probabilities overflow; its gradients must still be stored as
+    # zeros, and no other row may change beyond the bf16 bound.
+    layout = Layout(12, 16, 3, 64, 16, 4, 4)
+    q, k, v, do = inputs(layout.n_tot, 1, 2, head_dim, seed=31)
+    pad, (q2, k2, v2, do2) = fill_padding(layout, (q, k, v, do), seed=32)
+    for layer in (0, 1):
+        got = run_sparse(layout, layer, q2, k2, v2, do2, gpu)
+        for g in got:
+            assert np.all(g[:, :, pad] == 0), "padding gradients not zero"
+        ref = oracle(q, k, v, do, lambda rows: schedule.mask_rows(layout, layer, rows))
+        assert_grads(got, ref, "padding filled, layer %d" % layer)

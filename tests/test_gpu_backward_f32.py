@@ -108,3 +108,25 @@ def test_f32_and_bf16_backward_agree_to_bf16_rounding(gpu):
     b = run_sparse(layout, 1, *(t.float() for t in (q, k, v, do)), gpu)
     for x, y in zip(a, b):
         assert np.abs(x - y).max() <= BWD_MAX_REL * np.abs(y).max()
+
+
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_padding_slot_values_do_not_leak_into_gradients_f32(gpu, head_dim):
+    # large finite values in the padding slots of Q, K, V and dO: the
+    # padding gradients are zeros and every other gradient is unchanged
+    # (fp32 sums over the same keys in the same order: bit for bit)
+    layout = Layout(12, 16, 3, 64, 16, 4, 4)
+    q, k, v, do = inputs(layout.n_tot, 1, 2, head_dim, seed=33)
+    pad = layout.n_txt + np.nonzero(~schedule.valid_hilbert(layout))[0]
+    g = torch.Generator(device="cpu").manual_seed(34)
+    filled = []
+    for t in (q, k, v, do):
+        t = t.clone()
+        t[:, :, pad] = 300 * torch.randn(t[:, :, pad].shape, generator=g)
+        filled.append(t)
+    for layer in (0, 1):
+        clean = run_sparse(layout, layer, q, k, v, do, gpu)
+        got = run_sparse(layout, layer, *filled, gpu)
+        for a, b in zip(clean, got):
+            assert np.all(b[:, :, pad] == 0), "padding gradients not zero"
+            assert np.array_equal(a, b), "padding contents reached another row"

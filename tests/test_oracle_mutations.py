@@ -17,6 +17,7 @@ from oracle.schedule import Layout
 
 import test_oracle_accounting as t_acc
 import test_oracle_attention as t_att
+import test_oracle_attention_rows as t_rows
 import test_oracle_general as t_gen
 import test_oracle_gradients as t_grad
 import test_oracle_hilbert as t_hil
@@ -45,6 +46,9 @@ PINS = [
     lambda: t_att.test_global_rows_equal_dense_rows(),
     lambda: t_att.test_lse_is_logsumexp_of_unmasked_logits(),
     lambda: t_att.test_masked_keys_have_no_influence(),
+    lambda: t_rows.test_rows_equal_full_oracle_for_every_row_class(t_rows.LAYOUTS[0], 1),
+    lambda: t_rows.test_rows_equal_full_oracle_for_every_row_class(t_rows.LAYOUTS[2], 1),
+    lambda: t_rows.test_rows_match_the_loop_implementation(),
     lambda: t_tok.test_gather_orders_tokens_along_the_curve(8),
     lambda: t_tok.test_scatter_restores_raster_order(4),
     lambda: t_acc.test_nnz_matches_closed_form(Layout(16, 16, 0, 64, 32, 4, 4), 1, 22_368),
@@ -149,6 +153,33 @@ def _attention_with(mistake):
     return lambda orig: f
 
 
+def _rows_with(mistake):
+    """masked_attention_rows with one planted mistake."""
+    def f(q, k, v, rows, mask_rows, scale=None):
+        q, k, v = (np.asarray(a, dtype=np.float64) for a in (q, k, v))
+        d = q.shape[-1]
+        scale = 1.0 / math.sqrt(d) if scale is None else scale
+        if mistake == "no_scale":
+            scale = 1.0
+        rows = np.asarray(rows, dtype=np.int64)
+        m = np.asarray(mask_rows)
+        if mistake == "mask_row_offset":
+            m = np.roll(m, 1, axis=0)
+        some = m.any(axis=1)
+        s = np.einsum("bhid,bhjd->bhij", q[:, :, rows], k) * scale
+        s = np.where(m[None, None], s, -np.inf)
+        mx = np.where(some[None, None, :, None], s.max(axis=-1, keepdims=True), 0.0)
+        p = np.exp(s - mx)
+        den = p.sum(axis=-1, keepdims=True)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            o = np.einsum("bhij,bhjd->bhid", p, v) / den
+            ls = (mx + np.log(den))[..., 0]
+        if mistake == "empty_rows_not_zero":
+            return o, ls
+        return (np.where(some[None, None, :, None], o, 0.0), np.where(some[None, None, :], ls, -np.inf))
+    return lambda orig: f
+
+
 def _permute_through_inverse(orig):
     def f(x, perm):
         inv = np.empty_like(np.asarray(perm, dtype=np.int64))
@@ -235,6 +266,10 @@ MUTANTS = {
     "attention uses K for V": (attention, "masked_attention", _attention_with("k_for_v")),
     "attention not normalised": (attention, "masked_attention", _attention_with("no_normalise")),
     "lse without the max": (attention, "masked_attention", _attention_with("lse_without_max")),
+    "sampled rows: mask one row off": (attention, "masked_attention_rows", _rows_with("mask_row_offset")),
+    "sampled rows without scale": (attention, "masked_attention_rows", _rows_with("no_scale")),
+    "sampled rows: padding rows not empty": (
+        attention, "masked_attention_rows", _rows_with("empty_rows_not_zero")),
     "gather through the inverse": (tokens, "permute", _permute_through_inverse),
     "nnz drops the last row": (accounting, "nnz", _nnz_drops_last_block),
     "moved order is the plain curve": (schedule, "moved_perm", _moved_is_the_plain_curve),
