@@ -13,7 +13,8 @@ the closed form
 
 with masked entries excluded (weight exactly zero) and s the softmax scale
 (1/sqrt(D) unless given).  Rows are processed in blocks only to bound memory;
-each block is the plain formula.
+each block is the plain formula, its two products plain (BLAS) matrix
+products.
 """
 
 import math
@@ -25,7 +26,7 @@ def _as_f64(x):
     return np.asarray(x, dtype=np.float64)
 
 
-def masked_attention(q, k, v, mask_fn, scale=None, block=1024, empty_rows=False):
+def masked_attention(q, k, v, mask_fn, scale=None, block=256, empty_rows=False):
     """O and LSE for q, k, v of shape [B, H, N, D] (any float dtype, upcast).
 
     ``mask_fn(rows)`` returns the bool mask rows [len(rows), N]; the same mask
@@ -40,20 +41,21 @@ def masked_attention(q, k, v, mask_fn, scale=None, block=1024, empty_rows=False)
         scale = 1.0 / math.sqrt(d)
     out = np.empty((b, h, n, v.shape[-1]), dtype=np.float64)
     lse = np.empty((b, h, n), dtype=np.float64)
+    kt = np.ascontiguousarray(np.swapaxes(k, -1, -2))
     for r0 in range(0, n, block):
         rows = np.arange(r0, min(n, r0 + block))
         m = mask_fn(rows)
         some = m.any(axis=1)
         if not some.all() and not empty_rows:
             raise ValueError("every row must attend at least one key")
-        s = np.einsum("bhid,bhjd->bhij", q[:, :, rows], k) * scale
+        s = (q[:, :, rows] @ kt) * scale
         s = np.where(m[None, None], s, -np.inf)
         mx = s.max(axis=-1, keepdims=True)
         mx = np.where(some[None, None, :, None], mx, 0.0)
         p = np.exp(s - mx)
         den = p.sum(axis=-1, keepdims=True)
         with np.errstate(divide="ignore", invalid="ignore"):
-            o = np.einsum("bhij,bhjd->bhid", p, v) / den
+            o = (p @ v) / den
             ls = (mx + np.log(den))[..., 0]
         out[:, :, rows] = np.where(some[None, None, :, None], o, 0.0)
         lse[:, :, rows] = np.where(some[None, None, :], ls, -np.inf)
@@ -72,14 +74,14 @@ def masked_attention_rows(q, k, v, rows, mask_rows, scale=None):
         scale = 1.0 / math.sqrt(d)
     rows = np.asarray(rows, dtype=np.int64)
     some = np.asarray(mask_rows).any(axis=1)
-    s = np.einsum("bhid,bhjd->bhij", q[:, :, rows], k) * scale
+    s = (q[:, :, rows] @ np.swapaxes(k, -1, -2)) * scale
     s = np.where(mask_rows[None, None], s, -np.inf)
     mx = s.max(axis=-1, keepdims=True)
     mx = np.where(some[None, None, :, None], mx, 0.0)
     p = np.exp(s - mx)
     den = p.sum(axis=-1, keepdims=True)
     with np.errstate(divide="ignore", invalid="ignore"):
-        o = np.einsum("bhij,bhjd->bhid", p, v) / den
+        o = (p @ v) / den
         ls = (mx + np.log(den))[..., 0]
     return (np.where(some[None, None, :, None], o, 0.0),
             np.where(some[None, None, :], ls, -np.inf))
