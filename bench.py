@@ -20,7 +20,7 @@ the step time.
 Also reported, from the same process: per-call sparse and dense attention
 time at the 128^2 and 64^2 shapes, the speedup over the in-harness dense
 kernel, the gather's bandwidth, the roofline of the attention launch, and the
-oracle's rate on a bounded sample of the same workload.
+oracle's rate on one whole call of the 64x64 workload, on every host core.
 """
 
 import argparse
@@ -486,33 +486,39 @@ def main():
 
 
 def cpu_baseline(w):
-    """The float64 oracle on a bounded sample of the workload's rows."""
+    """The float64 oracle, as it stands, on one whole call of the 64 x 64
+    workload (24 heads, 4608 rows, layer 1) on every host core: its two
+    products are BLAS matrix products, run with one BLAS thread per core."""
     import numpy as np
     import torch
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     from oracle import attention, schedule
     from oracle.schedule import Layout
     from paper_2509_26538_amd import synth
 
-    layout = Layout(w.grid, w.grid, w.n_txt, w.tile, w.delta, w.shared, w.shared)
-    q, k, v = synth.qkv(w.batch, w.heads, w.n_tot, w.head_dim, w.dtype, seed=w.seed)
+    w64 = synth.WORKLOADS["flux-64"]
+    layout = Layout(w64.grid, w64.grid, w64.n_txt, w64.tile, w64.delta, w64.shared, w64.shared)
+    q, k, v = synth.qkv(w64.batch, w64.heads, w64.n_tot, w64.head_dim, w64.dtype, seed=w64.seed)
     q64, k64, v64 = (t.to(torch.float64).numpy() for t in (q, k, v))
-    n_rows = 320  # about 10 s of the oracle on one host core
-    rows = np.arange(0, w.n_tot, w.n_tot // n_rows)[:n_rows]
-    m = schedule.mask_rows(layout, 1, rows)
-    t0, c0 = time.perf_counter(), time.process_time()
-    attention.masked_attention_rows(q64, k64, v64, rows, m)
-    wall = time.perf_counter() - t0
-    cpu_s = time.process_time() - c0
-    flops = 4 * w.head_dim * w.batch * w.heads * int(m.sum())
+    threads = os.cpu_count()
+    with threadpool_limits(limits=threads, user_api="blas"):
+        blas = [p.get("num_threads") for p in threadpool_info() if p.get("user_api") == "blas"]
+        t0, c0 = time.perf_counter(), time.process_time()
+        attention.masked_attention(q64, k64, v64, lambda rows: schedule.mask_rows(layout, 1, rows))
+        wall = time.perf_counter() - t0
+        cpu_s = time.process_time() - c0
+    nnz = 0
+    for r0 in range(0, layout.n_tot, 1024):
+        nnz += int(schedule.mask_rows(layout, 1, np.arange(r0, min(layout.n_tot, r0 + 1024))).sum())
+    flops = 4 * w64.head_dim * w64.batch * w64.heads * nnz
     return {
         "value": flops / wall / 1e12,
         "unit": "TFLOP/s",
-        "cores": max(1, round(cpu_s / wall)),
+        "cores": round(cpu_s / wall, 1),
         "kind": "oracle",
-        "sample": "%d query rows (every %d-th of %d, all %d heads) of the 128x128 workload at "
-                  "layer 1; %.1f s wall, %.2f GFLOP visited" % (len(rows), w.n_tot // n_rows, w.n_tot,
-                                                                w.heads, wall, flops / 1e9),
+        "sample": "one whole call of the 64x64 + 512 text workload (24 heads x 4608 rows, D 128, layer 1); "
+                  "%.1f s wall, %.2f GFLOP visited; BLAS threads %s" % (wall, flops / 1e9, blas),
         "host_cpus": os.cpu_count(),
         "cpu_model": cpu_model(),
     }

@@ -150,3 +150,41 @@ def test_paper_table1_settings(gpu, name):
         r.check_rows(o, layer, sample_rows(r.layout, layer, n_random=8, seed=7), "%s layer %d" % (name, layer))
     del r
     torch.cuda.empty_cache()
+
+
+def test_flux64_every_row_of_every_head(gpu):
+    # The whole output of a flux-64 call (24 heads x 4608 rows x 128, layer
+    # 1: the slide puts the wrap tile at the end of the image span) against
+    # the oracle, element by element.  The oracle's full call takes about
+    # 10 s on 8 host cores.
+    import time
+    from attn_util import oracle_sparse
+    r = Resident("flux-64", gpu)
+    o = r.run(1).cpu().to(torch.float64).numpy()
+    t0 = time.time()
+    ro, _, ra = oracle_sparse(r.layout, 1, r.q, r.k, r.v)
+    print("oracle, full flux-64 call: %.1f s" % (time.time() - t0))
+    is_global, lab = schedule.token_classes(r.layout, 1)
+    img = lab[r.layout.n_txt:]
+    assert img[0] == img[-1], "layer 1 must have a wrap tile"
+    assert_close(o, ro, "bf16", "flux-64 layer 1, every row", absw=ra)
+
+
+def test_dense_unsplit_rows_at_flux128_length(gpu):
+    # the dense baseline as the benchmark times it at 128 x 128 + 512 text:
+    # 16896-key rows in one pass (no key chunks, no workspace)
+    w = synth.WORKLOADS["flux-128"]
+    n = w.n_txt + w.grid * w.grid
+    assert hb.dense_attn_workspace_bytes(w.batch, w.heads, n, w.head_dim, hb.HILBERTA_BF16) == 0
+    q, k, v = synth.qkv(w.batch, w.heads, n, w.head_dim, "bf16", seed=w.seed)
+    qd, kd, vd = (t.to(gpu) for t in (q, k, v))
+    o = torch.full_like(qd, float("nan"))
+    hb.dense_attn_fwd(qd, kd, vd, o)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(5)
+    rows = np.unique(np.concatenate([[0, 1, 511, 512, n // 2, n - 2, n - 1], rng.integers(0, n, 40)]))
+    hs = list(HEADS)
+    got = o[:, hs][:, :, rows].cpu().to(torch.float64).numpy()
+    ref, _, ra = oracle_rows(None, 0, q[:, hs], k[:, hs], v[:, hs], rows)
+    assert_close(got, ref, "bf16", "dense rows %s" % rows.tolist()[:8], absw=ra)
+    assert bool(torch.isfinite(o.float()).all())
