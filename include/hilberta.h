@@ -247,6 +247,34 @@ int hilberta_attn_bwd_workspace_bytes(const hilberta_config* cfg, int64_t batch,
                                       int64_t* bytes);
 
 /*
+ * hilberta_attn_fwd_noalloc -- hilberta_attn_fwd for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same kernels, results bit for bit
+ * those of hilberta_attn_fwd with a workspace, but the split key passes keep
+ * their partials in a device array the library owns (64 MiB per device,
+ * held from the library's load to the end of the process) instead of a
+ * caller workspace.  It calls no hipMalloc, hipFree or allocating library
+ * routine.  Arguments as for hilberta_attn_fwd, without the workspace; the
+ * stream must belong to the current device.
+ * Every call on one device shares that device's array: calls that overlap
+ * on one device (on different streams, or from different threads) race and
+ * give undefined results.
+ * Errors: as hilberta_attn_fwd; ECAPACITY when the split key passes would
+ * need more than the array holds (hilberta_attn_workspace_bytes > 64 MiB,
+ * e.g. 24 heads of a 256 x 256 grid); EINVAL when the stream belongs to
+ * another device than the current one.
+ */
+int hilberta_attn_fwd_noalloc(const hilberta_config* cfg, const int32_t* sched,
+                              const void* q, const void* k, const void* v,
+                              void* o, float* lse_or_null, int64_t batch,
+                              int64_t heads, int64_t head_dim,
+                              const int64_t q_strides[4],
+                              const int64_t k_strides[4],
+                              const int64_t v_strides[4],
+                              const int64_t o_strides[4], int dtype,
+                              float scale, void* stream);
+
+/*
  * hilberta_attn_bwd -- gradients of hilberta_attn_fwd's output with respect
  * to Q, K and V (the backward pass that training through the sparse
  * attention needs: §4.1 fine-tunes with LoRA, the appendix on training

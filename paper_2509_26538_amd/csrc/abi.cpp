@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "internal.hpp"
@@ -298,44 +299,112 @@ int check_workspace(const void* ws, int64_t ws_bytes) {
     return HILBERTA_OK;
 }
 
+// A validated attention call: its plan and launch description.  Built on the
+// host with no HIP call, so every argument error returns before anything is
+// launched.
+struct AttnCall {
+    Plan p;
+    hilberta::AttnArgs a;
+    bool empty;
+};
+
+int prepare_attention(bool sparse, const hilberta_config* cfg, const int32_t* sched, const void* q,
+                      const void* k, const void* v, void* o, float* lse, int64_t batch, int64_t heads,
+                      int64_t n_tot, int64_t head_dim, const int64_t* qs, const int64_t* ks,
+                      const int64_t* vs, const int64_t* os, int dtype, float scale, bool split,
+                      AttnCall& c) {
+    const Tensor4 t[4] = {{q, qs, "q"}, {k, ks, "k"}, {v, vs, "v"}, {o, os, "o"}};
+    c = AttnCall{};
+    int rc = attn_setup(sparse, cfg, sched, t, 4, batch, heads, n_tot, head_dim, dtype, scale, split, c.p,
+                        c.a, c.empty);
+    if (rc || c.empty) return rc;
+    c.a.lse = lse;
+    return HILBERTA_OK;
+}
+
+// The attention launch, then (split dense rows) the merge of the chunk
+// partials, which live in ws (at least c.p.ws_bytes).
+int launch_attention(AttnCall& c, int dtype, int64_t head_dim, void* ws, hipStream_t s) {
+    hilberta::AttnArgs& a = c.a;
+    a.ws = static_cast<float*>(ws);
+    int rc = hip_status(hilberta::launch_attn(a, dtype, (int)head_dim, s), "attention launch");
+    if (rc || c.p.n_chunks == 1) return rc;
+    hilberta::MergeArgs m{};
+    m.o = a.o;
+    m.lse = a.lse;
+    m.ws = a.ws;
+    m.sched = a.sched;
+    m.o_sb = a.o_sb; m.o_sh = a.o_sh; m.o_sr = a.o_sr;
+    m.heads = a.heads;
+    m.n_tot = a.n_tot;
+    m.n_txt = a.n_txt;
+    m.span_cap = a.span_cap;
+    m.n_dense_rows = a.n_dense_rows;
+    m.n_chunks = a.n_chunks;
+    m.n_bh = a.n_bh;
+    m.n_tiles = a.n_tiles;
+    m.sparse = a.sparse;
+    return hip_status(hilberta::launch_merge(m, dtype, (int)head_dim, s), "merge launch");
+}
+
 int run_attention(bool sparse, const hilberta_config* cfg, const int32_t* sched, const void* q,
                   const void* k, const void* v, void* o, float* lse, int64_t batch, int64_t heads,
                   int64_t n_tot, int64_t head_dim, const int64_t* qs, const int64_t* ks,
                   const int64_t* vs, const int64_t* os, int dtype, float scale, void* ws,
                   int64_t ws_bytes, void* stream) {
-    const Tensor4 t[4] = {{q, qs, "q"}, {k, ks, "k"}, {v, vs, "v"}, {o, os, "o"}};
     int rc = check_workspace(ws, ws_bytes);
     if (rc) return rc;
-    Plan p{};
-    hilberta::AttnArgs a{};
-    bool empty = false;
-    rc = attn_setup(sparse, cfg, sched, t, 4, batch, heads, n_tot, head_dim, dtype, scale, ws != nullptr, p, a,
-                    empty);
-    if (rc || empty) return rc;
-    if (ws && ws_bytes < p.ws_bytes)
+    AttnCall c;
+    rc = prepare_attention(sparse, cfg, sched, q, k, v, o, lse, batch, heads, n_tot, head_dim, qs, ks, vs, os,
+                           dtype, scale, ws != nullptr, c);
+    if (rc || c.empty) return rc;
+    if (ws && ws_bytes < c.p.ws_bytes)
         return fail(HILBERTA_ECAPACITY, "workspace of %lld bytes, %lld needed", (long long)ws_bytes,
-                    (long long)p.ws_bytes);
-    a.lse = lse;
-    a.ws = static_cast<float*>(ws);
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    rc = hip_status(hilberta::launch_attn(a, dtype, (int)head_dim, s), "attention launch");
-    if (rc || p.n_chunks == 1) return rc;
-    hilberta::MergeArgs m{};
-    m.o = o;
-    m.lse = lse;
-    m.ws = a.ws;
-    m.sched = sched;
-    m.o_sb = os[0]; m.o_sh = os[1]; m.o_sr = os[2];
-    m.heads = (int32_t)heads;
-    m.n_tot = (int32_t)n_tot;
-    m.n_txt = a.n_txt;
-    m.span_cap = a.span_cap;
-    m.n_dense_rows = (int32_t)p.n_dense_rows;
-    m.n_chunks = (int32_t)p.n_chunks;
-    m.n_bh = a.n_bh;
-    m.n_tiles = a.n_tiles;
-    m.sparse = a.sparse;
-    return hip_status(hilberta::launch_merge(m, dtype, (int)head_dim, s), "merge launch");
+                    (long long)c.p.ws_bytes);
+    return launch_attention(c, dtype, head_dim, ws, static_cast<hipStream_t>(stream));
+}
+
+// ------------------------------------------------- allocation-free forward
+// hilberta_attn_fwd_noalloc keeps the split key passes' partials in this
+// library-owned device array instead of a caller workspace.  Each device the
+// library runs on holds its own copy from module load to the end of the
+// process.  Host code never passes `scratch` itself to a kernel (on the host
+// it names a stand-in, not device memory): the device address of each
+// device's copy is taken once, with that device current, and kept here.
+// The partials are written in full before the merge reads them, so nothing
+// in the array has to start at zero.  Calls that overlap on one device share
+// the array and race.
+constexpr int64_t kScratchBytes = 64ll << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The scratch array's address on the device of `stream`, which must be the
+// current device.
+int scratch_on(void* stream, void** out) {
+    int cur = 0;
+    if (int rc = hip_status(hipGetDevice(&cur), "hipGetDevice")) return rc;
+    int dev = cur;
+    if (stream) {
+        hipDevice_t d = 0;
+        if (int rc = hip_status(hipStreamGetDevice(static_cast<hipStream_t>(stream), &d), "hipStreamGetDevice"))
+            return rc;
+        dev = d;
+    }
+    if (dev != cur)
+        return fail(HILBERTA_EINVAL, "the stream belongs to device %d but device %d is current", dev, cur);
+    if (dev < 0 || dev >= kMaxDevices) return fail(HILBERTA_EUNSUPPORTED, "device %d >= %d", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (int rc = hip_status(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)"))
+            return rc;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return HILBERTA_OK;
 }
 
 // Workspace of the backward: dO . O and the base-2 LSE per row, then the
@@ -548,6 +617,31 @@ int hilberta_attn_fwd(const hilberta_config* cfg, const int32_t* sched, const vo
     return run_attention(true, cfg, sched, q, k, v, o, lse_or_null, batch, heads, n_tot, head_dim,
                          q_strides, k_strides, v_strides, o_strides, dtype, scale, workspace,
                          workspace_bytes, stream);
+}
+
+int hilberta_attn_fwd_noalloc(const hilberta_config* cfg, const int32_t* sched, const void* q, const void* k,
+                              const void* v, void* o, float* lse_or_null, int64_t batch, int64_t heads,
+                              int64_t head_dim, const int64_t q_strides[4], const int64_t k_strides[4],
+                              const int64_t v_strides[4], const int64_t o_strides[4], int dtype, float scale,
+                              void* stream) {
+    int rc = check_config(cfg);
+    if (rc) return rc;
+    if (!sched) return fail(HILBERTA_EINVAL, "sched is NULL");
+    const int64_t n_tot = cfg->n_txt + span_len(cfg);
+    AttnCall c;
+    rc = prepare_attention(true, cfg, sched, q, k, v, o, lse_or_null, batch, heads, n_tot, head_dim, q_strides,
+                           k_strides, v_strides, o_strides, dtype, scale, true, c);
+    if (rc || c.empty) return rc;
+    if (c.p.ws_bytes > kScratchBytes)
+        return fail(HILBERTA_ECAPACITY,
+                    "the split key passes need %lld bytes, more than the %lld bytes of the library's scratch",
+                    (long long)c.p.ws_bytes, (long long)kScratchBytes);
+    void* ws = nullptr;
+    if (c.p.ws_bytes > 0) {
+        rc = scratch_on(stream, &ws);
+        if (rc) return rc;
+    }
+    return launch_attention(c, dtype, head_dim, ws, static_cast<hipStream_t>(stream));
 }
 
 int hilberta_attn_bwd_workspace_bytes(const hilberta_config* cfg, int64_t batch, int64_t heads,

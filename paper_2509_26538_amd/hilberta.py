@@ -27,7 +27,8 @@ EXPORTS = [
     "hilberta_version", "hilberta_last_error", "hilberta_build_perm",
     "hilberta_build_perm_layout", "hilberta_permute",
     "hilberta_unpermute", "hilberta_schedule_words", "hilberta_schedule",
-    "hilberta_attn_workspace_bytes", "hilberta_attn_fwd", "dense_attn_workspace_bytes",
+    "hilberta_attn_workspace_bytes", "hilberta_attn_fwd", "hilberta_attn_fwd_noalloc",
+    "dense_attn_workspace_bytes",
     "dense_attn_fwd", "hilberta_attn_bwd_workspace_bytes", "hilberta_attn_bwd",
     "dense_attn_bwd_workspace_bytes", "dense_attn_bwd",
 ]
@@ -76,6 +77,9 @@ def load(path=LIB_PATH):
         "hilberta_attn_fwd": (ctypes.c_int, [_CFGP, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64,
                                              _STR4, _STR4, _STR4, _STR4, ctypes.c_int,
                                              ctypes.c_float, _P, _I64, _P]),
+        "hilberta_attn_fwd_noalloc": (ctypes.c_int, [_CFGP, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64,
+                                                     _STR4, _STR4, _STR4, _STR4, ctypes.c_int,
+                                                     ctypes.c_float, _P]),
         "dense_attn_workspace_bytes": (ctypes.c_int, [_I64, _I64, _I64, _I64, ctypes.c_int, _I64P]),
         "dense_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _I64, _I64, _I64, _I64,
                                           _STR4, _STR4, _STR4, _STR4, ctypes.c_int,
@@ -254,6 +258,18 @@ def hilberta_attn_fwd(cfg, sched, q, k, v, o, lse=None, scale=None, workspace=No
                                     _ptr(o), _ptr(lse), b, h, d, _strides(q), _strides(k),
                                     _strides(v), _strides(o), _dtype(q), scale, wp, wb,
                                     _stream(stream)))
+
+
+def hilberta_attn_fwd_noalloc(cfg, sched, q, k, v, o, lse=None, scale=None, stream=None):
+    """hilberta_attn_fwd without a workspace: the library's own device array
+    holds the split partials (no allocation in the call)."""
+    b, h, n, d = q.shape
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    _same_dtype(q, k, v, o, lse)
+    _check(load().hilberta_attn_fwd_noalloc(ctypes.byref(cfg), _ptr(sched), _ptr(q), _ptr(k), _ptr(v),
+                                            _ptr(o), _ptr(lse), b, h, d, _strides(q), _strides(k),
+                                            _strides(v), _strides(o), _dtype(q), scale, _stream(stream)))
 
 
 def dense_attn_fwd(q, k, v, o, lse=None, scale=None, workspace=None, stream=None):

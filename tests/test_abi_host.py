@@ -166,6 +166,33 @@ def test_workspace_too_small_is_a_capacity_error(lib):
     assert str(need) in hb.last_error()
 
 
+def attn_noalloc(lib, cfg=None, b=1, h=2, d=64, dtype=hb.HILBERTA_BF16, scale=0.125, q=FAKE, o=FAKE,
+                 sched=FAKE, qs=None):
+    cfg = cfg or hb.make_config(16, 0, 64, 32, 4)
+    n = cfg.n_txt + hb.image_span(cfg.grid_h, cfg.grid_w)
+    s = strides(b, h, n, d)
+    return lib.hilberta_attn_fwd_noalloc(ctypes.byref(cfg), sched, q, FAKE, FAKE, o, None, b, h, d, qs or s, s,
+                                         s, s, dtype, scale, None)
+
+
+def test_noalloc_argument_errors_launch_nothing(lib):
+    # every check runs on the host before the library touches its device
+    # array (this machine has no GPU, so a HIP call would fail with EHIP)
+    assert attn_noalloc(lib, d=96) == hb.HILBERTA_EUNSUPPORTED
+    assert attn_noalloc(lib, q=None) == hb.HILBERTA_EINVAL
+    assert attn_noalloc(lib, sched=None) == hb.HILBERTA_EINVAL
+    assert attn_noalloc(lib, scale=0.0) == hb.HILBERTA_EINVAL
+    assert attn_noalloc(lib, q=FAKE + 8) == hb.HILBERTA_EUNSUPPORTED
+    assert attn_noalloc(lib, b=0) == hb.HILBERTA_OK  # nothing to do
+    # 24 heads of the 256 x 256 grid need ~190 MB of partials: more than the
+    # library's 64 MiB array holds
+    cfg = hb.make_config(256, 512, 2048, 1024, 32)
+    need = hb.hilberta_attn_workspace_bytes(cfg, 1, 24, 128, hb.HILBERTA_BF16)
+    assert need > 64 << 20
+    assert attn_noalloc(lib, cfg=cfg, h=24, d=128) == hb.HILBERTA_ECAPACITY
+    assert str(need) in hb.last_error()
+
+
 def test_dense_errors_and_workspace(lib):
     s = strides(1, 2, 100, 64)
     rc = lib.dense_attn_fwd(FAKE, FAKE, FAKE, FAKE, None, 1, 2, 100, 32, s, s, s, s,
