@@ -251,7 +251,7 @@ int hilberta_attn_bwd_workspace_bytes(const hilberta_config* cfg, int64_t batch,
  * allocate device memory (code under HIP graph capture, tight serving loops,
  * harnesses that forbid hipMalloc): the same kernels, results bit for bit
  * those of hilberta_attn_fwd with a workspace, but the split key passes keep
- * their partials in a device array the library owns (64 MiB per device,
+ * their partials in a device array the library owns (32 MiB per device,
  * held from the library's load to the end of the process) instead of a
  * caller workspace.  It calls no hipMalloc, hipFree or allocating library
  * routine.  Arguments as for hilberta_attn_fwd, without the workspace; the
@@ -260,9 +260,10 @@ int hilberta_attn_bwd_workspace_bytes(const hilberta_config* cfg, int64_t batch,
  * on one device (on different streams, or from different threads) race and
  * give undefined results.
  * Errors: as hilberta_attn_fwd; ECAPACITY when the split key passes would
- * need more than the array holds (hilberta_attn_workspace_bytes > 64 MiB,
- * e.g. 24 heads of a 256 x 256 grid); EINVAL when the stream belongs to
- * another device than the current one.
+ * need more than the array holds (hilberta_attn_workspace_bytes > 32 MiB;
+ * the Flux.1-dev shapes need at most 19 MB, a 64 x 64 grid with 2048 text
+ * tokens and 16 heads of D = 128 needs 36.6 MiB); EINVAL when the stream
+ * belongs to another device than the current one.
  */
 int hilberta_attn_fwd_noalloc(const hilberta_config* cfg, const int32_t* sched,
                               const void* q, const void* k, const void* v,

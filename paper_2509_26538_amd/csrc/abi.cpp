@@ -168,11 +168,14 @@ struct Plan {
         total_items, ws_bytes;
 };
 
-// Split long dense rows into key chunks about twice as long as a sparse
-// item's key list: no workgroup runs far longer than the rest (dense items
-// come first in their head's item range), and the partials stay few.  For
-// the dense baseline, split only when the rows alone would not fill the GPU
-// a few times.
+// HilbertA: dense rows (text and shared) attend every key.  Their keys are
+// split into chunks only as far as needed for no dense item to run longer
+// than a workgroup slot's share of the whole launch (the visited row blocks
+// x keys over 512 slots, two workgroups on each of 256 CUs), and never
+// shorter than twice a sparse item's key list: each XCD starts its dense
+// items first and its short sparse items fill the slots behind them, and the
+// partials to merge stay few.  For the dense baseline, split only when the
+// rows alone would not fill the GPU a few times.
 Plan make_plan(bool sparse, int64_t n_txt, int64_t n_img, int64_t n_shared, int64_t tile,
                int64_t n_tot, int64_t bh, int64_t head_dim, int dtype, bool allow_split) {
     Plan p{};
@@ -184,7 +187,12 @@ Plan make_plan(bool sparse, int64_t n_txt, int64_t n_img, int64_t n_shared, int6
         p.sparse_blocks = ceil_div(n_img, bm);
         const int64_t sparse_keys = round_up(n_txt, bn) + round_up(n_shared, bn) +
                                     round_up(tile < n_img ? tile : n_img, bn);
-        chunk = round_up(2 * (sparse_keys > 512 ? sparse_keys : 512), bn);
+        const int64_t work = bh * (ceil_div(p.n_dense_rows, bm) * n_tot + p.sparse_blocks * sparse_keys);
+        const int64_t share = ceil_div(work, 512);
+        const int64_t k = share > 0 ? ceil_div(n_tot, share) : 1;
+        chunk = round_up(ceil_div(n_tot, k), bn);
+        const int64_t floor_keys = round_up(2 * (sparse_keys > 512 ? sparse_keys : 512), bn);
+        if (chunk < floor_keys) chunk = floor_keys;
     } else {
         p.n_dense_rows = n_tot;
         p.sparse_blocks = 0;
@@ -374,7 +382,7 @@ int run_attention(bool sparse, const hilberta_config* cfg, const int32_t* sched,
 // The partials are written in full before the merge reads them, so nothing
 // in the array has to start at zero.  Calls that overlap on one device share
 // the array and race.
-constexpr int64_t kScratchBytes = 64ll << 20;
+constexpr int64_t kScratchBytes = 32ll << 20;
 constexpr int kMaxDevices = 64;
 static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 

@@ -100,9 +100,9 @@ __global__ void __launch_bounds__(kThreads, 1) attn_f32_kernel(AttnArgs a) {
     const int h = lane >> 5;
     const int ql = lane & 31;
 
-    const int item = remap_xcd(blockIdx.x, a.total_items);
-    const int32_t bh = item / a.items_per_bh;
-    const int32_t r = item - bh * a.items_per_bh;
+    const ItemId id = decode_item(blockIdx.x, a);
+    const int32_t bh = id.bh;
+    const int32_t r = id.r;
     const int32_t dense_items = a.dense_row_blocks * a.n_chunks;
     const bool dense = r < dense_items;
     MaskCtx mc{0, 0, 0, 0};

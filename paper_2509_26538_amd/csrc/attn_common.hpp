@@ -75,18 +75,47 @@ struct MaskCtx {
     int32_t o, r_start, r_len, label_mask;
 };
 
-__device__ __forceinline__ int remap_xcd(int pid, int total) {
-    // Workgroups are dealt to the 8 XCDs round-robin; give each XCD one
-    // contiguous range of logical items so the items of a (batch, head),
-    // which share K and V, meet in one L2.
+// Work item of workgroup pid: its (batch, head) slice bh and its index r
+// within the slice (r < dense_row_blocks * n_chunks: a dense item).  Items
+// of a slice are contiguous in the logical order (dense first), and the
+// logical order is dealt to the 8 XCDs in contiguous ranges, so the items of
+// a slice, which share K and V, meet in one L2.  Workgroups go to the XCDs
+// round-robin (pid mod 8); within its range an XCD takes every dense item
+// before any sparse one: the long items start first and the short ones fill
+// the end of the launch.
+struct ItemId {
+    int32_t bh, r;
+};
+
+__device__ __forceinline__ ItemId decode_item(int pid, const AttnArgs& a) {
     constexpr int X = 8;
+    const int total = a.total_items;
     const int per = (total + X - 1) / X;
     int tall = total % X;
     if (tall == 0) tall = X;
     const int xcd = pid % X;
     const int local = pid / X;
-    if (xcd < tall) return xcd * per + local;
-    return tall * per + (xcd - tall) * (per - 1) + local;
+    const int lo = xcd < tall ? xcd * per : tall * per + (xcd - tall) * (per - 1);
+    const int hi = lo + (xcd < tall ? per : per - 1);
+    const int ipb = a.items_per_bh;
+    const int di = a.dense_row_blocks * a.n_chunks;  // dense items per slice
+    const int si = ipb - di;
+    // dense items before logical position x
+    auto dense_before = [&](int x) { return (x / ipb) * di + min(x % ipb, di); };
+    const int fl = dense_before(lo);
+    const int nd = dense_before(hi) - fl;
+    int item;
+    if (local < nd) {  // the range holds a dense item, so di > 0
+        const int k = fl + local;
+        item = (k / di) * ipb + k % di;
+    } else {  // and here a sparse one, so si > 0
+        const int k = (lo - fl) + (local - nd);
+        item = (k / si) * ipb + di + k % si;
+    }
+    ItemId id;
+    id.bh = item / ipb;
+    id.r = item - id.bh * ipb;
+    return id;
 }
 
 __device__ __forceinline__ int32_t shared_seq(const Spans& sp, int32_t u) {

@@ -184,13 +184,17 @@ def test_noalloc_argument_errors_launch_nothing(lib):
     assert attn_noalloc(lib, scale=0.0) == hb.HILBERTA_EINVAL
     assert attn_noalloc(lib, q=FAKE + 8) == hb.HILBERTA_EUNSUPPORTED
     assert attn_noalloc(lib, b=0) == hb.HILBERTA_OK  # nothing to do
-    # 24 heads of the 256 x 256 grid need ~190 MB of partials: more than the
-    # library's 64 MiB array holds
-    cfg = hb.make_config(256, 512, 2048, 1024, 32)
-    need = hb.hilberta_attn_workspace_bytes(cfg, 1, 24, 128, hb.HILBERTA_BF16)
-    assert need > 64 << 20
-    assert attn_noalloc(lib, cfg=cfg, h=24, d=128) == hb.HILBERTA_ECAPACITY
+    # a 64 x 64 grid with 2048 text tokens and 16 heads needs 36.6 MiB of
+    # partials: more than the library's 32 MiB array holds
+    cfg = hb.make_config(64, 2048, 256, 128, 16)
+    need = hb.hilberta_attn_workspace_bytes(cfg, 1, 16, 128, hb.HILBERTA_BF16)
+    assert need > 32 << 20
+    assert attn_noalloc(lib, cfg=cfg, h=16, d=128) == hb.HILBERTA_ECAPACITY
     assert str(need) in hb.last_error()
+    # the Flux.1-dev workloads fit
+    for g, tile, shared in ((64, 256, 8), (128, 1024, 16), (256, 2048, 32)):
+        cfg = hb.make_config(g, 512, tile, tile // 2, shared)
+        assert hb.hilberta_attn_workspace_bytes(cfg, 1, 24, 128, hb.HILBERTA_BF16) <= 32 << 20
 
 
 def test_dense_errors_and_workspace(lib):

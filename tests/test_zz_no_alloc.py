@@ -28,7 +28,7 @@ def test_noalloc_matches_the_workspace_entry_point(gpu):
         cfg, sched = make_schedule(layout, layer, gpu)
         q, k, v = (t.to(gpu) for t in synth.qkv(b, h, layout.n_tot, d, dtype, seed=layout.n_tot + d))
         need = hb.hilberta_attn_workspace_bytes(cfg, b, h, d, hb._dtype(q))
-        assert 0 < need <= 64 << 20  # the split path, within the library's array
+        assert 0 < need <= 32 << 20  # the split path, within the library's array
         o_ref = torch.full_like(q, float("nan"))
         l_ref = torch.full((b, h, layout.n_tot), float("nan"), dtype=torch.float32, device=gpu)
         hb.hilberta_attn_fwd(cfg, sched, q, k, v, o_ref, l_ref, workspace=workspace(need, gpu))
