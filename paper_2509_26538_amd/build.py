@@ -1,10 +1,16 @@
 """Build libhilberta.so in-tree with hipcc for gfx950.
 
-    python -m paper_2509_26538_amd.build [-v]
+    python -m paper_2509_26538_amd.build [-v] [--sanitize]
 
 Each source compiles to an object under ``_build/`` (in parallel), then the
 objects link into ``paper_2509_26538_amd/libhilberta.so``.  Every call
 recompiles.
+
+``--sanitize`` builds ``_build/asan/libhilberta.so`` instead: the same
+library with the host code of the C ABI (argument checks, plans, launches)
+compiled with AddressSanitizer and UndefinedBehaviorSanitizer; device code is
+not instrumented.  Load it with the ASan runtime preloaded
+(``sanitizer_runtime()``) and ``HILBERTA_LIB`` pointing at it.
 """
 
 import concurrent.futures
@@ -30,9 +36,15 @@ COMMON = [
 ]
 
 
-def _compile(src, verbose):
-    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC] + COMMON + ["-c", os.path.join(CSRC, src), "-o", obj]
+# host-only sanitizers: each -fsanitize= is bound to the host compilation
+SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
+ASAN_DIR = os.path.join(BUILD, "asan")
+
+
+def _compile(src, verbose, out_dir=BUILD, extra=()):
+    obj = os.path.join(out_dir, os.path.splitext(src)[0] + ".o")
+    cmd = [HIPCC] + COMMON + list(extra) + ["-c", os.path.join(CSRC, src), "-o", obj]
     if src.endswith(".cpp"):
         cmd[1:1] = ["-x", "hip"]
     if verbose:
@@ -62,5 +74,32 @@ def build(verbose=False):
     return LIB
 
 
+def build_sanitized(verbose=False):
+    """_build/asan/libhilberta.so: abi.cpp's host code under ASan and UBSan."""
+    os.makedirs(ASAN_DIR, exist_ok=True)
+
+    def one(src):
+        return _compile(src, verbose, ASAN_DIR, SANITIZE if src == "abi.cpp" else ())
+
+    with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
+        objs = list(ex.map(one, SOURCES))
+    lib = os.path.join(ASAN_DIR, "libhilberta.so")
+    cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-Xarch_host", "-fsanitize=address",
+           "-Xarch_host", "-fsanitize=undefined", "-o", lib] + objs
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("link failed:\n" + r.stderr)
+    return lib
+
+
+def sanitizer_runtime():
+    """Path of the ASan runtime the sanitized library needs preloaded."""
+    r = subprocess.run([HIPCC, "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True, text=True)
+    return r.stdout.strip()
+
+
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    if "--sanitize" in sys.argv:
+        print(build_sanitized(verbose="-v" in sys.argv))
+    else:
+        print(build(verbose="-v" in sys.argv))

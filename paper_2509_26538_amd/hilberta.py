@@ -21,7 +21,9 @@ SCHEDULE_MAGIC = 0x48424131
 LAYOUT_IN_PLACE = 0
 LAYOUT_MOVED = 1
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhilberta.so")
+# the in-tree build; HILBERTA_LIB names another build of the same library
+# (the host-sanitized one of build.build_sanitized, for the ABI tests)
+LIB_PATH = os.environ.get("HILBERTA_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhilberta.so")
 
 EXPORTS = [
     "hilberta_version", "hilberta_last_error", "hilberta_build_perm",
