@@ -172,13 +172,20 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
                 dma16(vrs, vl + j * 1024, vb0 + voff[j]);
             }
         } else {
+            // every key row first, then the loads: each load is an asm
+            // statement with a memory clobber, so a shared-token map read
+            // (LDS) placed after one could not start before it
+            int32_t key[G::IPW];
 #pragma unroll
             for (int j = 0; j < G::IPW; ++j) {
                 // absent rows of a ragged stage re-read a present row (masked)
                 const int32_t rr = min(srow[j], cnt - 1);
-                const int32_t key = base >= 0 ? base + rr : list_seq(v0 + rr, b1, b2, b3, s0, sa, sb, sm.sp);
-                dma16(krs, kl + j * 1024, key * krow_b + kcol[j]);
-                dma16(vrs, vl + j * 1024, key * vrow_b + vcol[j]);
+                key[j] = base >= 0 ? base + rr : list_seq(v0 + rr, b1, b2, b3, s0, sa, sb, sm.sp);
+            }
+#pragma unroll
+            for (int j = 0; j < G::IPW; ++j) {
+                dma16(krs, kl + j * 1024, key[j] * krow_b + kcol[j]);
+                dma16(vrs, vl + j * 1024, key[j] * vrow_b + vcol[j]);
             }
         }
         if (!PAD && !stage_fast(i) && tid < kBN) {

@@ -260,17 +260,22 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
             if (none) return;
         }
         const uint32_t off = buf * SB;
+        // every key row first, then the loads (an asm statement with a
+        // memory clobber each: a map read after one could not start before it)
+        int32_t key[IPW];
 #pragma unroll
         for (int j = 0; j < IPW; ++j) {
-            int32_t key;
             if (base >= 0 && cnt == kBQ) {
-                key = base + srow[j];
+                key[j] = base + srow[j];
             } else {
                 const int32_t rr = min(srow[j], cnt - 1);
-                key = base >= 0 ? base + rr : list_seq(v0 + rr, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
+                key[j] = base >= 0 ? base + rr : list_seq(v0 + rr, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
             }
-            dma16(krs, k0 + off + j * 1024, key * krow_b + colk[j]);
-            dma16(vrs, v0l + off + j * 1024, key * vrow_b + colk[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < IPW; ++j) {
+            dma16(krs, k0 + off + j * 1024, key[j] * krow_b + colk[j]);
+            dma16(vrs, v0l + off + j * 1024, key[j] * vrow_b + colk[j]);
         }
         if (!PAD && !stage_fast(i) && tid < kBQ) {
             const int32_t v = v0 + tid;
@@ -467,17 +472,21 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
             srow[j] = p / G::CPR;
             colk[j] = ((p % G::CPR) ^ G::fk(srow[j])) * 16;
             }
+        // every query row first, then the loads (see the dQ pass)
+        int32_t qs[IPW];
 #pragma unroll
         for (int j = 0; j < IPW; ++j) {
-            int32_t qs;
             if (base >= 0 && cnt == kBQ) {
-                qs = base + srow[j];
+                qs[j] = base + srow[j];
             } else {
                 const int32_t rr = min(srow[j], cnt - 1);
-                qs = base >= 0 ? base + rr : list_seq(v0 + rr, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
+                qs[j] = base >= 0 ? base + rr : list_seq(v0 + rr, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
             }
-            dma16(qrs, q0 + off + j * 1024, qs * qrow_b + colk[j]);
-            dma16(drs, d0 + off + j * 1024, qs * drow_b + colk[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < IPW; ++j) {
+            dma16(qrs, q0 + off + j * 1024, qs[j] * qrow_b + colk[j]);
+            dma16(drs, d0 + off + j * 1024, qs[j] * drow_b + colk[j]);
         }
         if (!PAD && !stage_fast(i) && tid < kBQ) sm.info[buf][tid] = entry_info<false>(a, L, v, seq, o, sm.sp);
     };
