@@ -164,12 +164,13 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
             if (none) return;  // nothing but padding: not loaded, not computed
         }
         if (base >= 0 && cnt == kBN) {
-            // a full stage of contiguous keys: one uniform offset
+            // a full stage of contiguous keys (inside the slice: every
+            // segment of the list lies in [0, n_tot)): one uniform offset
             const int32_t kb0 = base * krow_b, vb0 = base * vrow_b;
 #pragma unroll
             for (int j = 0; j < G::IPW; ++j) {
-                dma16(krs, kl + j * 1024, kb0 + koff[j]);
-                dma16(vrs, vl + j * 1024, vb0 + voff[j]);
+                dma16s(krs, kl + j * 1024, koff[j], kb0);
+                dma16s(vrs, vl + j * 1024, voff[j], vb0);
             }
         } else {
             // every key row first, then the loads: each load is an asm

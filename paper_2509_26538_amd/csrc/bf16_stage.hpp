@@ -61,6 +61,18 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rsrc, uint32_t lds_
                  : "memory", "m0");
 }
 
+// The same with a uniform byte offset in the instruction's scalar offset
+// field, for a stage of contiguous rows: the per-lane offset stays fixed for
+// the whole item, so issuing the stage costs no vector instruction.  The
+// scalar offset is outside the buffer's range check; callers use it only
+// for rows that lie inside the slice.
+__device__ __forceinline__ void dma16s(__amdgpu_buffer_rsrc_t rsrc, uint32_t lds_base, int32_t voff, int32_t soff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :
+                 : "s"(lds_base), "v"(voff), "s"(rsrc), "s"(soff)
+                 : "memory", "m0");
+}
+
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void*)p);
 }
