@@ -93,6 +93,10 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
     const bool label_mask = L.label_mask;
     const int nblk = (total + kBN - 1) / kBN;
     RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
+    // a wavefront whose 32 rows all lie past the dense rows (the last dense
+    // block when the dense rows are not a multiple of 128) only stages its
+    // share of the keys: its SIMD is left to the other workgroup
+    const bool idle = dense && row0 + wave * 32 >= a.n_dense_rows;
     if (!PAD) ri.pad = false;
 
     const int32_t bb = bh / a.heads;
@@ -318,9 +322,19 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
         wait_vmcnt<0>();
         __syncthreads();
     };
-    for (int32_t i = 0; i < nblk; i += 2) {
-        stage(i, std::integral_constant<int, 0>{});
-        if (i + 1 < nblk) stage(i + 1, std::integral_constant<int, 1>{});
+    if (idle) {
+        // only this wavefront's share of every stage's loads, and the
+        // barriers the other wavefronts wait at
+        for (int32_t i = 0; i < nblk; ++i) {
+            if (i + 1 < nblk) load_stage(i + 1, (i + 1) & 1);
+            wait_vmcnt<0>();
+            __syncthreads();
+        }
+    } else {
+        for (int32_t i = 0; i < nblk; i += 2) {
+            stage(i, std::integral_constant<int, 0>{});
+            if (i + 1 < nblk) stage(i + 1, std::integral_constant<int, 1>{});
+        }
     }
 
     __bf16* obase = reinterpret_cast<__bf16*>(a.o) + bb * a.o_sb + hh * a.o_sh;

@@ -159,7 +159,14 @@ __device__ __forceinline__ int32_t entry_info(const AttnArgs& a, const ItemList&
                                               int32_t o, const Spans& sp) {
     if (v >= L.total) return kKeyInvalid;
     if (PAD && seq_padding(a, seq)) return kKeyInvalid;
-    if (L.label_mask && v >= L.b2 && !is_shared_seq(sp, seq)) return tile_label(seq - a.n_txt, o, a.tile, a.n_img);
+    if (L.label_mask && v >= L.b2 && !is_shared_seq(sp, seq)) {
+        // the divisors pass through an empty asm statement, so that the
+        // compiler forms their reciprocals here, on this rarely taken path,
+        // instead of holding them in registers across the whole stage loop
+        int32_t tile = a.tile, n_img = a.n_img;
+        asm volatile("" : "+s"(tile), "+s"(n_img));
+        return tile_label(seq - a.n_txt, o, tile, n_img);
+    }
     return kKeyAll;
 }
 
