@@ -189,6 +189,10 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
     const ItemList L = item_list(a, dense, chunk, row0, o, n_shared, sm.sp, sm.n_keep, wave, lane);
     const int nblk = (L.total + kBQ - 1) / kBQ;
     RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
+    // a wavefront whose 32 rows all lie past the dense rows (the last dense
+    // block when the dense rows are not a multiple of 128) only stages its
+    // share of the list: its SIMD is left to the other workgroup
+    const bool idle = dense && row0 + wave * 32 >= a.n_dense_rows;
     if (!PAD) ri.pad = false;
 
     const int32_t bb = bh / a.heads;
@@ -340,9 +344,18 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
         wait_vmcnt<0>();
         __syncthreads();
     };
-    for (int32_t i = 0; i < nblk; i += 2) {
-        stage(i, std::integral_constant<int, 0>{});
-        if (i + 1 < nblk) stage(i + 1, std::integral_constant<int, 1>{});
+    if (idle) {
+        // never wavefront 0, which also publishes the stages' row values
+        for (int32_t i = 0; i < nblk; ++i) {
+            if (i + 1 < nblk) load_stage(i + 1, (i + 1) & 1);
+            wait_vmcnt<0>();
+            __syncthreads();
+        }
+    } else {
+        for (int32_t i = 0; i < nblk; i += 2) {
+            stage(i, std::integral_constant<int, 0>{});
+            if (i + 1 < nblk) stage(i + 1, std::integral_constant<int, 1>{});
+        }
     }
     if (dense && a.n_chunks > 1) {
         store_partial<D>(a, bh, chunk, ri.dense_row, 0, acc, h);
@@ -391,6 +404,10 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
     const ItemList L = item_list(a, dense, chunk, row0, o, n_shared, sm.sp, sm.n_keep, wave, lane);
     const int nblk = (L.total + kBQ - 1) / kBQ;
     RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
+    // a wavefront whose 32 rows all lie past the dense rows (the last dense
+    // block when the dense rows are not a multiple of 128) only stages its
+    // share of the list: its SIMD is left to the other workgroup
+    const bool idle = dense && row0 + wave * 32 >= a.n_dense_rows;
     if (!PAD) ri.pad = false;
 
     const int32_t bb = bh / a.heads;
@@ -578,9 +595,18 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
         }
         __syncthreads();
     };
-    for (int32_t i = 0; i < nblk; i += 2) {
-        stage(i, std::integral_constant<int, 0>{});
-        if (i + 1 < nblk) stage(i + 1, std::integral_constant<int, 1>{});
+    if (idle) {
+        // never wavefront 0, which also publishes the stages' row values
+        for (int32_t i = 0; i < nblk; ++i) {
+            if (i + 1 < nblk) load_stage(i + 1, (i + 1) & 1);
+            wait_vmcnt<0>();
+            __syncthreads();
+        }
+    } else {
+        for (int32_t i = 0; i < nblk; i += 2) {
+            stage(i, std::integral_constant<int, 0>{});
+            if (i + 1 < nblk) stage(i + 1, std::integral_constant<int, 1>{});
+        }
     }
     if (dense && a.n_chunks > 1) {
         store_partial<D>(a, bh, chunk, ri.dense_row, 0, acck, h);
