@@ -206,21 +206,22 @@ __global__ void __launch_bounds__(kThreads, 1) attn_f32_kernel(AttnArgs a) {
 // Merge of the split key chunks of dense rows: with chunk partials
 // (acc_c, m_c, l_c), M = max m_c, L = sum l_c 2^(m_c - M) and
 // O = sum acc_c 2^(m_c - M) / L -- the same rescaling Algorithm 1 applies
-// between key blocks.  One wavefront per row.
-// Split-K merge of the dense rows.  A row is handled by 32 lanes, each owning
-// four consecutive elements (16-byte loads); a wavefront merges two rows.
-// The chunks' (m, l) are read by one lane per chunk and combined with
-// cross-lane reductions; the partial accumulators are streamed with
-// non-temporal loads, four chunks in flight.
+// between key blocks, taken here chunk by chunk as an online merge.  A row
+// is handled by D/4 lanes, each owning four consecutive elements (16-byte
+// loads); every lane reads the (m, l) of every chunk itself (the lanes of a
+// row read the same words), so no cross-lane step waits between the loads:
+// the partials of four chunks are requested at once, non-temporal.
 template <typename T, int D>
 __global__ void __launch_bounds__(256) merge_kernel(MergeArgs m) {
+    typedef float f4 __attribute__((ext_vector_type(4)));
     constexpr int LPR = D / 4;  // lanes per row
     constexpr int RPB = 256 / LPR;
+    constexpr int CH = 4;       // chunks in flight
     const int sub = threadIdx.x % LPR;
     const int64_t rowid = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
-    const bool valid_row = rowid < (int64_t)m.n_bh * m.n_dense_rows;
-    const int32_t bh = valid_row ? (int32_t)(rowid / m.n_dense_rows) : 0;
-    const int32_t r = valid_row ? (int32_t)(rowid - (int64_t)bh * m.n_dense_rows) : 0;
+    if (rowid >= (int64_t)m.n_bh * m.n_dense_rows) return;
+    const int32_t bh = (int32_t)(rowid / m.n_dense_rows);
+    const int32_t r = (int32_t)(rowid - (int64_t)bh * m.n_dense_rows);
     int32_t seq = r;
     if (m.sparse && r >= m.n_txt) {
         const int32_t n_sp = min(max(m.sched[6], 0), min(m.span_cap, kMaxSpans));
@@ -236,54 +237,44 @@ __global__ void __launch_bounds__(256) merge_kernel(MergeArgs m) {
             }
             u -= ln;
         }
+        if (seq < 0) return;
     }
-    const bool active = valid_row && seq >= 0;
     const float* ml = m.ws + (int64_t)m.n_bh * m.n_chunks * m.n_dense_rows * D;
     const int64_t slot0 = (int64_t)bh * m.n_chunks * m.n_dense_rows + r;
-    // global max of the chunks' m, then L = sum_c 2^(m_c - M) l_c
-    float mx = -INFINITY;
-    for (int32_t c = sub; c < m.n_chunks; c += LPR)
-        if (active) mx = fmaxf(mx, ml[(slot0 + (int64_t)c * m.n_dense_rows) * 2]);
-#pragma unroll
-    for (int off = LPR / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, LPR));
-    const float m_use = mx == -INFINITY ? 0.f : mx;
-    float L = 0.f;
-    for (int32_t c = sub; c < m.n_chunks; c += LPR) {
-        if (!active) break;
-        const int64_t slot = slot0 + (int64_t)c * m.n_dense_rows;
-        L += __builtin_amdgcn_exp2f(ml[slot * 2] - m_use) * ml[slot * 2 + 1];
-    }
-#pragma unroll
-    for (int off = LPR / 2; off > 0; off >>= 1) L += __shfl_xor(L, off, LPR);
-    typedef float f4 __attribute__((ext_vector_type(4)));
+    float M = -INFINITY, L = 0.f;
     f4 o = {0.f, 0.f, 0.f, 0.f};
-    if (active) {
-        int32_t c = 0;
-        for (; c + 4 <= m.n_chunks; c += 4) {
-            f4 part[4];
-            float w[4];
+    for (int32_t c0 = 0; c0 < m.n_chunks; c0 += CH) {
+        float mc[CH], lc[CH];
+        f4 part[CH];
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const int64_t slot = slot0 + (int64_t)(c + k) * m.n_dense_rows;
+        for (int k = 0; k < CH; ++k) {
+            mc[k] = -INFINITY;
+            lc[k] = 0.f;
+            part[k] = f4{0.f, 0.f, 0.f, 0.f};
+            if (c0 + k < m.n_chunks) {
+                const int64_t slot = slot0 + (int64_t)(c0 + k) * m.n_dense_rows;
+                mc[k] = ml[slot * 2];
+                lc[k] = ml[slot * 2 + 1];
                 part[k] = __builtin_nontemporal_load(reinterpret_cast<const f4*>(m.ws + slot * D) + sub);
-                w[k] = __builtin_amdgcn_exp2f(ml[slot * 2] - m_use);
             }
-#pragma unroll
-            for (int k = 0; k < 4; ++k) o += w[k] * part[k];
         }
-        for (; c < m.n_chunks; ++c) {
-            const int64_t slot = slot0 + (int64_t)c * m.n_dense_rows;
-            const f4 part = __builtin_nontemporal_load(reinterpret_cast<const f4*>(m.ws + slot * D) + sub);
-            o += __builtin_amdgcn_exp2f(ml[slot * 2] - m_use) * part;
+#pragma unroll
+        for (int k = 0; k < CH; ++k) {
+            // a chunk (or the running sum) with m = -inf carries weight 0
+            const float mn = fmaxf(M, mc[k]);
+            const float mu = mn == -INFINITY ? 0.f : mn;
+            const float wa = __builtin_amdgcn_exp2f(M - mu), wb = __builtin_amdgcn_exp2f(mc[k] - mu);
+            L = L * wa + lc[k] * wb;
+            o = o * wa + part[k] * wb;
+            M = mn;
         }
     }
-    if (!active) return;
     const float inv = L > 0.f ? 1.f / L : 0.f;
     const int32_t b = bh / m.heads, hh = bh - b * m.heads;
     T* orow = reinterpret_cast<T*>(m.o) + b * m.o_sb + hh * m.o_sh + (int64_t)seq * m.o_sr;
     store4<T>(orow + 4 * sub, o[0] * inv, o[1] * inv, o[2] * inv, o[3] * inv);
     if (m.lse && sub == 0)
-        m.lse[(int64_t)bh * m.n_tot + seq] = L > 0.f ? (m_use + log2f(L)) * kLn2 : -INFINITY;
+        m.lse[(int64_t)bh * m.n_tot + seq] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
 }
 template <int D>
 hipError_t launch_f32(const AttnArgs& a, hipStream_t s) {
