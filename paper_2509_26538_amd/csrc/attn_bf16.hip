@@ -93,10 +93,12 @@ __global__ void __launch_bounds__(kThreads, 2) attn_bf16_kernel(AttnArgs a) {
     const bool label_mask = L.label_mask;
     const int nblk = (total + kBN - 1) / kBN;
     RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
-    // a wavefront whose 32 rows all lie past the dense rows (the last dense
-    // block when the dense rows are not a multiple of 128) only stages its
-    // share of the keys: its SIMD is left to the other workgroup
-    const bool idle = dense && row0 + wave * 32 >= a.n_dense_rows;
+    // a wavefront that stores none of its 32 rows (rows past the dense rows
+    // in the last dense block, a sparse block's rows of shared tokens, which
+    // dense items own, or rows past the image span) only stages its share of
+    // the keys: its SIMD is left to the other workgroup.  Every duty of
+    // wavefront 0 beyond that lies in load_stage, which it still runs.
+    const bool idle = __builtin_amdgcn_ballot_w64(ri.store) == 0;
     if (!PAD) ri.pad = false;
 
     const int32_t bb = bh / a.heads;

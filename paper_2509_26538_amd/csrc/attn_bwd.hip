@@ -189,10 +189,11 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
     const ItemList L = item_list(a, dense, chunk, row0, o, n_shared, sm.sp, sm.n_keep, wave, lane);
     const int nblk = (L.total + kBQ - 1) / kBQ;
     RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
-    // a wavefront whose 32 rows all lie past the dense rows (the last dense
-    // block when the dense rows are not a multiple of 128) only stages its
-    // share of the list: its SIMD is left to the other workgroup
-    const bool idle = dense && row0 + wave * 32 >= a.n_dense_rows;
+    // a wavefront that stores none of its 32 rows (rows past the dense rows
+    // in the last dense block, a sparse block's rows of shared tokens, which
+    // dense items own, or rows past the image span) only stages its share of
+    // the list: its SIMD is left to the other workgroup
+    const bool idle = __builtin_amdgcn_ballot_w64(ri.store) == 0;
     if (!PAD) ri.pad = false;
 
     const int32_t bb = bh / a.heads;
@@ -345,7 +346,6 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
         __syncthreads();
     };
     if (idle) {
-        // never wavefront 0, which also publishes the stages' row values
         for (int32_t i = 0; i < nblk; ++i) {
             if (i + 1 < nblk) load_stage(i + 1, (i + 1) & 1);
             wait_vmcnt<0>();
@@ -404,10 +404,12 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
     const ItemList L = item_list(a, dense, chunk, row0, o, n_shared, sm.sp, sm.n_keep, wave, lane);
     const int nblk = (L.total + kBQ - 1) / kBQ;
     RowInfo ri = row_info(a, dense, row0, wave * 32 + ql, kBlockMBf16, o, n_shared, sm.sp);
-    // a wavefront whose 32 rows all lie past the dense rows (the last dense
-    // block when the dense rows are not a multiple of 128) only stages its
-    // share of the list: its SIMD is left to the other workgroup
-    const bool idle = dense && row0 + wave * 32 >= a.n_dense_rows;
+    // a wavefront that stores none of its 32 rows (rows past the dense rows
+    // in the last dense block, a sparse block's rows of shared tokens, which
+    // dense items own, or rows past the image span) only stages its share of
+    // the list: its SIMD is left to the other workgroup.  Not wavefront 0,
+    // which also publishes each stage's row values.
+    const bool idle = wave != 0 && __builtin_amdgcn_ballot_w64(ri.store) == 0;
     if (!PAD) ri.pad = false;
 
     const int32_t bb = bh / a.heads;
@@ -596,7 +598,6 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
         __syncthreads();
     };
     if (idle) {
-        // never wavefront 0, which also publishes the stages' row values
         for (int32_t i = 0; i < nblk; ++i) {
             if (i + 1 < nblk) load_stage(i + 1, (i + 1) & 1);
             wait_vmcnt<0>();
