@@ -239,7 +239,10 @@ int hilberta_attn_fwd(const hilberta_config* cfg, const int32_t* sched,
 /*
  * hilberta_attn_bwd_workspace_bytes -- device workspace hilberta_attn_bwd
  * needs: 8 bytes per row of every (batch, head), for dO . O and the LSE in
- * log2 units.  Host only.  Errors: as hilberta_schedule_words for cfg;
+ * log2 units, plus, when the rows that attend every key are split into key
+ * chunks, 8 D bytes per such row, chunk and (batch, head) for the fp32
+ * partial sums (of dQ in the first pass, of dK and dV in the second).
+ * Host only.  Errors: as hilberta_schedule_words for cfg;
  * EUNSUPPORTED (head_dim, dtype other than bf16).
  */
 int hilberta_attn_bwd_workspace_bytes(const hilberta_config* cfg, int64_t batch,
