@@ -37,31 +37,44 @@ namespace {
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 // Dlt_i = dO_i . O_i in fp32 and lse2_i = LSE_i log2(e) (0 for a row that
-// attends nothing, whose probabilities are all masked anyway).  D/4 lanes
-// per row, four elements each.
+// attends nothing, whose probabilities are all masked anyway).  D/8 lanes
+// per row, eight elements (one 16-byte load of each tensor) each; a block
+// covers kPrepPasses groups of 256/(D/8) consecutive rows and requests all
+// of their loads before the first sum.
+constexpr int kPrepPasses = 4;
+
 template <int D>
 __global__ void __launch_bounds__(256) bwd_prep_kernel(AttnArgs a, BwdArgs g) {
-    constexpr int LPR = D / 4;
-    constexpr int RPB = 256 / LPR;
+    constexpr int LPR = D / 8;
+    constexpr int RPP = 256 / LPR;
+    typedef __bf16 bf16x8v __attribute__((ext_vector_type(8)));
     const int sub = threadIdx.x % LPR;
-    const int64_t rowid = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
     const int64_t rows = (int64_t)a.n_bh * a.n_tot;
-    const bool ok = rowid < rows;
-    const int64_t r = ok ? rowid : 0;
-    const int64_t bh = r / a.n_tot, n = r - bh * a.n_tot;
-    const int64_t b = bh / a.heads, hh = bh - b * a.heads;
-    const int64_t off = b * a.o_sb + hh * a.o_sh + n * a.o_sr + 4 * sub;
-    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-    const bf16x4 o4 = *reinterpret_cast<const bf16x4*>(reinterpret_cast<const __bf16*>(a.o) + off);
-    const bf16x4 d4 = *reinterpret_cast<const bf16x4*>(reinterpret_cast<const __bf16*>(g.dout) + off);
-    float t = (float)o4[0] * (float)d4[0] + (float)o4[1] * (float)d4[1] + (float)o4[2] * (float)d4[2] +
-              (float)o4[3] * (float)d4[3];
+    const int64_t first = (int64_t)blockIdx.x * (RPP * kPrepPasses) + threadIdx.x / LPR;
+    bf16x8v o8[kPrepPasses], d8[kPrepPasses];
 #pragma unroll
-    for (int w = LPR / 2; w > 0; w >>= 1) t += __shfl_xor(t, w, LPR);
-    if (ok && sub == 0) {
-        g.delta[r] = t;
-        const float l = g.lse[r];
-        g.lse2[r] = l == -INFINITY ? 0.f : l * 1.4426950408889634f;
+    for (int u = 0; u < kPrepPasses; ++u) {
+        const int64_t rowid = first + u * RPP;
+        const int64_t r = rowid < rows ? rowid : 0;
+        const int64_t bh = r / a.n_tot, n = r - bh * a.n_tot;
+        const int64_t b = bh / a.heads, hh = bh - b * a.heads;
+        const int64_t off = b * a.o_sb + hh * a.o_sh + n * a.o_sr + 8 * sub;
+        o8[u] = *reinterpret_cast<const bf16x8v*>(reinterpret_cast<const __bf16*>(a.o) + off);
+        d8[u] = *reinterpret_cast<const bf16x8v*>(reinterpret_cast<const __bf16*>(g.dout) + off);
+    }
+#pragma unroll
+    for (int u = 0; u < kPrepPasses; ++u) {
+        float t = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) t += (float)o8[u][e] * (float)d8[u][e];
+#pragma unroll
+        for (int w = LPR / 2; w > 0; w >>= 1) t += __shfl_xor(t, w, LPR);
+        const int64_t r = first + u * RPP;
+        if (r < rows && sub == 0) {
+            g.delta[r] = t;
+            const float l = g.lse[r];
+            g.lse2[r] = l == -INFINITY ? 0.f : l * 1.4426950408889634f;
+        }
     }
 }
 
@@ -230,12 +243,14 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
     // direct loads: lane l of load j fills LDS chunk p = (w IPW + j) 64 + l
     // of the stage, i.e. row p / CPR, stored chunk p % CPR, which holds
     // global chunk (p % CPR) ^ f(row)
-    int32_t srow[IPW], colk[IPW];
+    int32_t srow[IPW], colk[IPW], koff[IPW], voff[IPW];
 #pragma unroll
     for (int j = 0; j < IPW; ++j) {
         const int p = (wave * IPW + j) * 64 + lane;
         srow[j] = p / G::CPR;
         colk[j] = ((p % G::CPR) ^ G::fk(srow[j])) * 16;
+        koff[j] = srow[j] * krow_b + colk[j];  // byte offset within a stage of consecutive rows
+        voff[j] = srow[j] * vrow_b + colk[j];
     }
     const uint32_t k0 = lds_addr(&sm.k[0][wave * IPW * 1024]);
     const uint32_t v0l = lds_addr(&sm.v[0][wave * IPW * 1024]);
@@ -265,22 +280,29 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
             if (none) return;
         }
         const uint32_t off = buf * SB;
-        // every key row first, then the loads (an asm statement with a
-        // memory clobber each: a map read after one could not start before it)
-        int32_t key[IPW];
+        if (base >= 0 && cnt == kBQ) {
+            // 32 consecutive rows inside the slice: the first row's byte
+            // offset goes in the scalar offset field
 #pragma unroll
-        for (int j = 0; j < IPW; ++j) {
-            if (base >= 0 && cnt == kBQ) {
-                key[j] = base + srow[j];
-            } else {
+            for (int j = 0; j < IPW; ++j) {
+                dma16s(krs, k0 + off + j * 1024, koff[j], base * krow_b);
+                dma16s(vrs, v0l + off + j * 1024, voff[j], base * vrow_b);
+            }
+        } else {
+            // every key row first, then the loads (an asm statement with a
+            // memory clobber each: a map read after one could not start
+            // before it)
+            int32_t key[IPW];
+#pragma unroll
+            for (int j = 0; j < IPW; ++j) {
                 const int32_t rr = min(srow[j], cnt - 1);
                 key[j] = base >= 0 ? base + rr : list_seq(v0 + rr, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
             }
-        }
 #pragma unroll
-        for (int j = 0; j < IPW; ++j) {
-            dma16(krs, k0 + off + j * 1024, key[j] * krow_b + colk[j]);
-            dma16(vrs, v0l + off + j * 1024, key[j] * vrow_b + colk[j]);
+            for (int j = 0; j < IPW; ++j) {
+                dma16(krs, k0 + off + j * 1024, key[j] * krow_b + colk[j]);
+                dma16(vrs, v0l + off + j * 1024, key[j] * vrow_b + colk[j]);
+            }
         }
         if (!PAD && !stage_fast(i) && tid < kBQ) {
             const int32_t v = v0 + tid;
@@ -482,30 +504,36 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
         const uint32_t off = buf * SB;
         // row and swizzled chunks of this lane's piece of load j, formed per
         // stage (cheaper than holding them across the loop)
-        int lane_s = lane;
+        uint32_t lane_s = lane;
         asm volatile("" : "+v"(lane_s));
         int32_t srow[IPW], colk[IPW];
 #pragma unroll
         for (int j = 0; j < IPW; ++j) {
-            const int p = (wave * IPW + j) * 64 + lane_s;
-            srow[j] = p / G::CPR;
-            colk[j] = ((p % G::CPR) ^ G::fk(srow[j])) * 16;
-            }
-        // every query row first, then the loads (see the dQ pass)
-        int32_t qs[IPW];
+            const uint32_t p = (uint32_t)(wave * IPW + j) * 64u + lane_s;
+            srow[j] = (int32_t)(p / G::CPR);
+            colk[j] = (int32_t)(((p % G::CPR) ^ (uint32_t)G::fk(srow[j])) * 16u);
+        }
+        if (base >= 0 && cnt == kBQ) {
+            // 32 consecutive rows inside the slice: the first row's byte
+            // offset goes in the scalar offset field
 #pragma unroll
-        for (int j = 0; j < IPW; ++j) {
-            if (base >= 0 && cnt == kBQ) {
-                qs[j] = base + srow[j];
-            } else {
+            for (int j = 0; j < IPW; ++j) {
+                dma16s(qrs, q0 + off + j * 1024, srow[j] * qrow_b + colk[j], base * qrow_b);
+                dma16s(drs, d0 + off + j * 1024, srow[j] * drow_b + colk[j], base * drow_b);
+            }
+        } else {
+            // every query row first, then the loads (see the dQ pass)
+            int32_t qs[IPW];
+#pragma unroll
+            for (int j = 0; j < IPW; ++j) {
                 const int32_t rr = min(srow[j], cnt - 1);
                 qs[j] = base >= 0 ? base + rr : list_seq(v0 + rr, L.b1, L.b2, L.b3, L.s0, L.sa, L.sb, sm.sp);
             }
-        }
 #pragma unroll
-        for (int j = 0; j < IPW; ++j) {
-            dma16(qrs, q0 + off + j * 1024, qs[j] * qrow_b + colk[j]);
-            dma16(drs, d0 + off + j * 1024, qs[j] * drow_b + colk[j]);
+            for (int j = 0; j < IPW; ++j) {
+                dma16(qrs, q0 + off + j * 1024, qs[j] * qrow_b + colk[j]);
+                dma16(drs, d0 + off + j * 1024, qs[j] * drow_b + colk[j]);
+            }
         }
         if (!PAD && !stage_fast(i) && tid < kBQ) sm.info[buf][tid] = entry_info<false>(a, L, v, seq, o, sm.sp);
     };
@@ -623,7 +651,8 @@ template <int D>
 hipError_t launch_bwd_t(const AttnArgs& a, const BwdArgs& g, hipStream_t s) {
     const int64_t rows = (int64_t)a.n_bh * a.n_tot;
     constexpr int64_t rpb = 256 / (D / 4);
-    const int64_t pblocks = (rows + rpb - 1) / rpb;
+    constexpr int64_t ppb = 256 / (D / 8) * kPrepPasses;
+    const int64_t pblocks = (rows + ppb - 1) / ppb;
     if (pblocks > 0x7fffffff) return hipErrorInvalidValue;
     hipLaunchKernelGGL((bwd_prep_kernel<D>), dim3((unsigned)pblocks), dim3(256), 0, s, a, g);
     hipError_t e = hipGetLastError();
