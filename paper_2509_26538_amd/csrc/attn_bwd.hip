@@ -332,13 +332,32 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dq_kernel(AttnArgs a, BwdArgs
             const uint8_t* vb_ = sm.v[buf];
             // S^T = K Q^T and dP^T = V dO^T: register e holds key
             // 8 (e/4) + 4 h + e%4 against this lane's row
+            // K and V operands requested kAhead reduction steps before use
             f32x16 s = f32x16{}, dp = ndlt16;
+            constexpr int kAhead = 3;
+            bf16x8 rk[kAhead + 1], rv[kAhead + 1];
+#pragma unroll
+            for (int kc = 0; kc < kAhead; ++kc) {
+                rk[kc] = *reinterpret_cast<const bf16x8*>(kb_ + (ka ^ (32 * kc)));
+                rv[kc] = *reinterpret_cast<const bf16x8*>(vb_ + (ka ^ (32 * kc)));
+            }
 #pragma unroll
             for (int kc = 0; kc < D / 16; ++kc) {
-                const int ad = ka ^ (32 * kc);
-                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(kb_ + ad), q[kc], s, 0, 0, 0);
-                dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(vb_ + ad), dov[kc], dp, 0,
-                                                             0, 0);
+                if (kc + kAhead < D / 16) {
+                    const int ad = ka ^ (32 * (kc + kAhead));
+                    rk[(kc + kAhead) % (kAhead + 1)] = *reinterpret_cast<const bf16x8*>(kb_ + ad);
+                    rv[(kc + kAhead) % (kAhead + 1)] = *reinterpret_cast<const bf16x8*>(vb_ + ad);
+                }
+                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(rk[kc % (kAhead + 1)], q[kc], s, 0, 0, 0);
+                dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(rv[kc % (kAhead + 1)], dov[kc], dp, 0, 0, 0);
+            }
+            // keep that order: the scheduler would otherwise sink each read
+            // to just before its product
+            __builtin_amdgcn_sched_group_barrier(0x100, 2 * kAhead, 0);
+#pragma unroll
+            for (int kc = 0; kc < D / 16; ++kc) {
+                if (kc + kAhead < D / 16) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
             }
             if (PAD ? sm.slow[buf] != 0 : !stage_fast(i)) {
 #pragma unroll
@@ -608,15 +627,26 @@ __global__ void __launch_bounds__(kThreads, 2) bwd_dkdv_kernel(AttnArgs a, BwdAr
                 }
             const uint8_t* dtb = sm.d[buf];
             const uint8_t* qtb = sm.q[buf];
+            // the phase's products in a fixed order (m = 4 D/32 cc... : dV^T
+            // for even m, dK^T for odd m), each A operand requested
+            // kAhead products before its use
+            constexpr int NM = 2 * 2 * (D / 32);
+            constexpr int kAhead = 2;
+            auto opnd = [&](int m) -> bf16x8 {
+                return tr_operand<D>((m & 1) ? qtb : dtb, va0_s, va1_s, m / (2 * (D / 32)), (m >> 1) % (D / 32));
+            };
+            bf16x8 ring[kAhead + 1];
 #pragma unroll
-            for (int cc = 0; cc < 2; ++cc)
+            for (int m = 0; m < kAhead; ++m) ring[m] = opnd(m);
 #pragma unroll
-                for (int dt = 0; dt < D / 32; ++dt) {
-                    accv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(dtb, va0_s, va1_s, cc, dt), pb[cc],
-                                                                       accv[dt], 0, 0, 0);
-                    acck[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(qtb, va0_s, va1_s, cc, dt), ds[cc],
-                                                                       acck[dt], 0, 0, 0);
-                }
+            for (int m = 0; m < NM; ++m) {
+                if (m + kAhead < NM) ring[(m + kAhead) % (kAhead + 1)] = opnd(m + kAhead);
+                const int cc = m / (2 * (D / 32)), dt = (m >> 1) % (D / 32);
+                if (m & 1)
+                    acck[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[m % (kAhead + 1)], ds[cc], acck[dt], 0, 0, 0);
+                else
+                    accv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[m % (kAhead + 1)], pb[cc], accv[dt], 0, 0, 0);
+            }
         }
         wait_vmcnt<0>();
         if (wave == 0 && lane < kBQ && i + 1 < nblk) {
