@@ -112,6 +112,33 @@ def test_logit_scale_drifting_along_the_keys_bf16(gpu, order):
     assert np.abs(dl - rl).max() <= 1e-3
 
 
+@pytest.mark.parametrize("factor", [12.0, 60.0])
+def test_logit_jump_past_the_reference_bf16(gpu, factor):
+    # Every 97th key is scaled up, so that a row's logits jump, somewhere in
+    # its key list, far above the reference max the kernel formed from its
+    # first keys: by tens of log2 units at factor 12 (the stage's
+    # probabilities stay finite but huge) and by well over 128 at factor 60
+    # (exp2 overflows to inf against the old reference).  Either way the
+    # stage must be redone from its own row max.  The rows are then
+    # dominated by one or two keys, |O| stays below ~4.
+    layout = Layout(32, 32, 40, 128, 64, 6, 6)
+    q, k, v = inputs(layout, 1, 2, 128, "bf16", seed=23)
+    scale = torch.ones(layout.n_tot, dtype=torch.float32)
+    scale[50::97] = factor
+    k = (k.float() * scale[None, None, :, None]).to(torch.bfloat16)
+    for layer in (0, 1):
+        for split in (False, True):
+            o, lse = hip_sparse(layout, layer, q, k, v, gpu, split=split)
+            ro, rl, ra = oracle_sparse(layout, layer, q, k, v)
+            what = "x%g layer %d split %s" % (factor, layer, split)
+            assert_close(o, ro, "bf16", what, absw=ra)
+            assert np.abs(lse - rl).max() <= 1e-3, what
+    od, dl = hip_dense(q, k, v, gpu)
+    ro, rl, ra = oracle_rows(None, 0, q, k, v, np.arange(layout.n_tot))
+    assert_close(od, ro, "bf16", "x%g dense" % factor, absw=ra)
+    assert np.abs(dl - rl).max() <= 1e-3
+
+
 def test_one_tile_equals_dense(gpu):
     # §3.2 with N_T = N_img: a single tile is dense attention
     layout = Layout(32, 32, 21, 1024, 256, 6, 6)
