@@ -5,7 +5,7 @@
 //   Dlt_i = dO_i . O_i,   dP = dO V^T,   dS = P (dP - Dlt),
 //   dV = P^T dO,          dK = s dS^T Q,   dQ = s dS K.
 // bf16 inputs and gradients, fp32 MFMA accumulation, P and dS rounded to
-// bf16 as MFMA operands.  Three launches:
+// bf16 as MFMA operands.  The launches:
 //   bwd_prep_kernel  Dlt and the LSE in log2 units, one per row;
 //   bwd_dq_kernel    the forward's query items and key lists: per stage
 //                    S^T = K Q^T and dP^T = V dO^T with the keys as A
@@ -16,7 +16,9 @@
 //                    is symmetric); S = Q K^T and dP = dO V^T with the
 //                    queries as A operands (one key row per lane), then
 //                    dV^T += dO^T P and dK^T += Q^T dS with Q and dO read
-//                    transposed.
+//                    transposed;
+//   bwd_sum_kernel   after each pass, when rows are split over key (query)
+//                    chunks: the sum of the chunk partials.
 // No atomics: every gradient row is written once by the item that owns it,
 // so the results are deterministic.  Rows that attend every key (text and
 // shared rows) and keys every query attends are items of their own over the
